@@ -1,0 +1,135 @@
+/*
+ * acrl_oracle.h -- CPU oracle for the ACRL scoring / discrepancy path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This library is the slow, plain, fp64 statement
+ * of what the GPU path must compute.  Only the test suite, the smoke check and
+ * the benchmark's CPU-baseline leg may load it.  It shares no code, header,
+ * table or helper with the HIP library; the two are independent on purpose.
+ *
+ * Every array argument is a HOST pointer.  Floating point is double unless
+ * the definition being followed fixes fp32 (the quantizer's scale and divide).
+ * Return value of the int functions: 0 on success, -1 on a bad argument.
+ *
+ * Citations name the section / equation of the ACRL paper
+ * ("Adaptive Control of Training-Inference Discrepancy for Stable RL").
+ */
+#ifndef ACRL_ORACLE_H
+#define ACRL_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Scaling granularity of the FP8 inference policy mu (Sec. 5.1 setup: per-token
+ * activations, per-channel weights; Sec. 5.2 / 5.4: MXFP8).                  */
+enum { REF_PER_TENSOR = 0, REF_PER_ROW = 1, REF_MX32 = 2 };
+/* Rounding of the FP8 encoder: nearest (Sec. 5.1 "nearest-around") or the
+ * truncation used in the stress test, Q(x) = trunc(x/S) (Sec. 5.3).          */
+enum { REF_ROUND_NEAREST_EVEN = 0, REF_ROUND_TOWARD_ZERO = 1 };
+/* Granularity of Y in alpha = gamma*sign(A)*(1 - Y/X) (Sec. 4.1).            */
+enum { REF_Y_GROUP = 0, REF_Y_SEQUENCE = 1, REF_Y_BATCH = 2 };
+
+/* Indices into the batch statistics vector written by the reduce. */
+enum {
+  REF_STAT_Y_BATCH = 0,        /* mean over non-empty groups of Y_g            */
+  REF_STAT_TOK_MEAN_D = 1,     /* token-level mean of d over valid tokens      */
+  REF_STAT_TOK_MAX_D = 2,      /* token-level max of d                         */
+  REF_STAT_TOK_STD_D = 3,      /* token-level population std of d              */
+  REF_STAT_MEAN_H_PI = 4,      /* mean entropy of pi over valid tokens         */
+  REF_STAT_MEAN_H_MU = 5,      /* mean entropy of mu over valid tokens         */
+  REF_STAT_N_TOKENS = 6,       /* number of valid tokens                       */
+  REF_STAT_N_GROUPS = 7,       /* number of non-empty groups                   */
+  REF_STAT_TOK_MEAN_LOGRATIO = 8, /* token-level mean of log(pi/mu)            */
+  REF_STAT_N_SEQS = 9,         /* number of non-empty sequences                */
+  REF_N_STATS = 10
+};
+
+/* ---- number formats -------------------------------------------------- */
+float   acrl_ref_bf16_to_float(uint16_t bits);
+/* OCP FP8 E4M3 ("fn": bias 7, max 448, S.1111.111 = NaN, no infinities).
+ * Nearest-even or toward-zero; magnitudes >= 448 (and infinities) saturate
+ * to +-448; NaN -> 0x7F with the input's sign.                              */
+uint8_t acrl_ref_e4m3_encode(float x, int rounding);
+double  acrl_ref_e4m3_decode(uint8_t code);
+/* OCP E8M0 shared scale: 2^(code-127); code 255 is NaN.                     */
+double  acrl_ref_e8m0_decode(uint8_t code);
+void    acrl_ref_e4m3_encode_array(const float* x, int64_t n, int rounding, uint8_t* out);
+
+/* ---- a1/a2: FP8 quantization of a bf16 matrix ------------------------- *
+ * x: bf16 bits [rows, ld] (cols used).  q: [rows, cols] codes.
+ * scales: float[1] (PER_TENSOR), float[rows] (PER_ROW),
+ *         uint8 e8m0 [rows, cols/32] (MX32, cols % 32 == 0).               */
+int acrl_ref_quantize_fp8(const uint16_t* x, int64_t rows, int64_t cols, int64_t ld,
+                          int scaling, int rounding, uint8_t* q, void* scales);
+
+/* ---- a3/a4: logits of one token over the whole vocabulary -------------- */
+int acrl_ref_logits_pi(const uint16_t* h_row, const uint16_t* w, int64_t d, int64_t V,
+                       double inv_temperature, double* z);
+/* hq_row: codes of the token; row_scale: pointer to this token's scale
+ * (float for PER_TENSOR/PER_ROW, d/32 e8m0 bytes for MX32).  wq_scales is the
+ * weight scale array as produced by acrl_ref_quantize_fp8 for W.            */
+int acrl_ref_logits_mu(const uint8_t* hq_row, const void* row_scale, const uint8_t* wq,
+                       const void* wq_scales, int scaling, int64_t d, int64_t V,
+                       double inv_temperature, double* z);
+
+/* ---- a3..a5: log-softmax statistics of one token ---------------------- */
+void acrl_ref_token_stats(const double* z, int64_t V, int32_t id,
+                          double* lse, double* logp, double* entropy);
+
+/* ---- a3..a5 for many rows: both policies ----------------------------- *
+ * Row r of h / hq is scored with sampled id ids[r].  Rows with mask[r]==0
+ * (mask may be NULL = all valid) get all outputs 0.  Outputs are [n_rows]
+ * doubles; every output pointer except logp_pi/logp_mu may be NULL.
+ * hq_scales: float[1] / float[n_rows] / uint8 [n_rows, d/32].              */
+int acrl_ref_score(int64_t n_rows, int64_t d, int64_t V,
+                   const uint16_t* h, const uint16_t* w,
+                   const uint8_t* hq, const void* hq_scales,
+                   const uint8_t* wq, const void* wq_scales, int scaling,
+                   const int32_t* ids, const uint8_t* mask, double inv_temperature,
+                   double* logp_pi, double* logp_mu, double* ent_pi, double* ent_mu,
+                   double* lse_pi, double* lse_mu, double* z_pi, double* z_mu);
+
+/* ---- a6/a7: per-token discrepancy and the segmented masked reduce ------ *
+ * Slot (i, j) = i*L + j.  ent_pi/ent_mu may be NULL (means reported as 0).
+ * Outputs: d_tok[B*L] (0 where masked), seq_len[B], seq_sum_d[B],
+ * seq_sum_logratio[B], seq_mean_d[B] (0 for empty sequences),
+ * group_y[n_groups] (0 for empty groups), group_nseq[n_groups] (non-empty
+ * sequences per group), stats[REF_N_STATS].  Any output may be NULL.       */
+int acrl_ref_discrepancy_reduce(int64_t B, int64_t L,
+                                const double* logp_pi, const double* logp_mu,
+                                const double* ent_pi, const double* ent_mu,
+                                const uint8_t* mask, const int32_t* group_of_seq, int64_t n_groups,
+                                double* d_tok, int32_t* seq_len, double* seq_sum_d,
+                                double* seq_sum_logratio, double* seq_mean_d,
+                                double* group_y, int32_t* group_nseq, double* stats);
+
+/* ---- a8: the ACRL controller step ------------------------------------ *
+ * adv: [B] (one advantage per response, GRPO) or [B*L] (adv_per_token=1).
+ * Y is read from seq_mean_d[i], group_y[group_of_seq[i]] or stats[0]
+ * according to y_level.  Outputs alpha, weight [B*L]; masked slots -> 0.
+ * Requires X > 0, gamma > 0, C > 1.                                        */
+int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
+                             const int32_t* group_of_seq,
+                             const double* logp_pi, const double* logp_mu,
+                             const double* adv, int adv_per_token, int y_level,
+                             const double* seq_mean_d, const double* group_y,
+                             const double* stats, double X, double gamma, double C,
+                             double* alpha, double* weight);
+
+/* Reference X (Sec. 4.1): mean of the per-group discrepancy over the
+ * non-empty groups (group_nseq > 0) of the step-0 batches.                 */
+int acrl_ref_reference_x(const double* group_y, const int32_t* group_nseq, int64_t n_groups,
+                         double* X);
+
+/* ---- fixture helper (not part of the method): inverse-CDF sampling ----- *
+ * Samples one id per row from softmax(z_row) using the supplied uniform
+ * u[r] in [0,1): the smallest v whose cumulative probability exceeds u.     */
+int acrl_ref_sample_inverse_cdf(const double* z, int64_t n_rows, int64_t V,
+                                const double* u, int32_t* ids);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
