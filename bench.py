@@ -1,0 +1,247 @@
+"""Benchmark: scored tokens/s of the ACRL scoring path on one MI355X.
+
+One step = the whole hot path over one batch already resident in HBM:
+quantize H for mu (per-tensor FP8), score every valid token under pi (BF16)
+and mu (FP8) with the fused log-softmax, merge, reduce the discrepancy per
+sequence / group / batch, and apply the ACRL controller.  W's quantization
+happens once per weight version and is reported separately.
+
+Usage: python bench.py [--gpus 1] [--steps 5] [--warmup 2] [--workload q8b]
+Prints progress on stderr and ONE JSON line on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+import inputs
+
+PEAK_TFLOPS = {"bf16": 2500.0, "fp8": 5000.0}   # MI355X dense MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="q8b", choices=sorted(inputs.WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="approximate CPU time budget of the oracle baseline (0 = skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this path runs on a single MI355X "
+              "(multi-GPU sharding is design-only); use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2607_24062_amd import acrl
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    acrl.lib()
+    w = inputs.WORKLOADS[args.workload]
+    T = inputs.n_valid(w)
+    d, V = w.d, w.V
+    log("workload:", w.describe(), "| valid tokens", T, "of", w.slots, "slots")
+
+    # ---------------- inputs resident in HBM
+    t0 = time.time()
+    H = inputs.hidden_bf16_torch(w, T, dev)
+    W = inputs.weights_bf16_torch(w, dev)
+    ids = torch.from_numpy(inputs.uniform_ids(w, T)).to(dev)
+    slots = torch.from_numpy(inputs.valid_slots(w)).to(dev)
+    mask = torch.from_numpy(inputs.mask(w).reshape(-1)).to(dev)
+    groups = torch.from_numpy(inputs.group_of_seq(w)).to(dev)
+    adv = torch.from_numpy(inputs.advantages(w)).to(dev)
+    torch.cuda.synchronize()
+    log("inputs generated in %.1fs" % (time.time() - t0))
+
+    # ---------------- W quantization (once per weight version)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    a, b = ev(), ev()
+    a.record()
+    wq, ws = acrl.acrl_quantize_fp8(W, w.scaling)
+    b.record()
+    torch.cuda.synchronize()
+    a.record()
+    wq, ws = acrl.acrl_quantize_fp8(W, w.scaling, q=wq, scales=ws)
+    b.record()
+    torch.cuda.synchronize()
+    wq_ms = a.elapsed_time(b)
+    wq_bytes = V * d * (2 + 1) + (V * d * 2 if w.scaling == inputs.PER_TENSOR else 0)
+    log("quantize W: %.3f ms (%.0f GB/s)" % (wq_ms, wq_bytes / wq_ms / 1e6))
+
+    # ---------------- preallocated step buffers
+    hq = torch.empty((T, d), dtype=torch.uint8, device=dev)
+    if w.scaling == inputs.PER_TENSOR:
+        hs = torch.empty(1, dtype=torch.float32, device=dev)
+    elif w.scaling == inputs.PER_ROW:
+        hs = torch.empty(T, dtype=torch.float32, device=dev)
+    else:
+        hs = torch.empty((T, d // 32), dtype=torch.uint8, device=dev)
+    outs = {k: torch.zeros(w.slots, dtype=torch.float32, device=dev)
+            for k in ("logp_pi", "logp_mu", "entropy_pi", "entropy_mu")}
+    X_ref = [None]
+
+    def step(trace_events=None, qev=None, rev=None):
+        if qev is not None:
+            qev[0].record()
+        acrl.acrl_quantize_fp8(H, w.scaling, q=hq, scales=hs)
+        if qev is not None:
+            qev[1].record()
+        if trace_events is not None:
+            acrl.acrl_trace_score_events(trace_events)
+        sc = acrl.acrl_score_pi_mu(H, W, hq, hs, wq, ws, w.scaling, ids,
+                                   inv_temperature=w.inv_temperature, out_slot=slots,
+                                   n_slots=w.slots, outputs=outs, want=("entropy",))
+        if trace_events is not None:
+            acrl.acrl_trace_score_events(None)
+        if rev is not None:
+            rev[0].record()
+        red = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, sc["logp_pi"], sc["logp_mu"], mask,
+                                           groups, entropy_pi=sc["entropy_pi"],
+                                           entropy_mu=sc["entropy_mu"], want_d_tok=False)
+        if rev is not None:
+            rev[1].record()
+        # X: the step-0 batch discrepancy (read once, outside the timed steps)
+        X = X_ref[0] if X_ref[0] is not None else 1.0
+        acrl.acrl_controller_step(w.B, w.L, w.n_prompts, mask, groups, sc["logp_pi"], sc["logp_mu"],
+                                  adv, False, acrl.Y_GROUP, red["seq_mean_d"], red["group_y"],
+                                  red["stats"], X, 0.65, 3.0, want_alpha=False)
+        if rev is not None:
+            rev[2].record()
+        return red
+
+    # ---------------- warmup (step 0 calibrates X, Sec. 4.1)
+    t0 = time.time()
+    red = step()
+    torch.cuda.synchronize()
+    X_ref[0] = max(float(red["stats"][0].item()), 1e-12)
+    for _ in range(max(args.warmup - 1, 0)):
+        step()
+    torch.cuda.synchronize()
+    log("warmup %d steps in %.1fs; X = %.4g" % (args.warmup, time.time() - t0, X_ref[0]))
+
+    # ---------------- timed steps (whole path), then per-kernel event timing
+    start, end = ev(), ev()
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / args.steps
+
+    K = args.steps
+    tev = [[ev() for _ in range(4)] for _ in range(K)]
+    qev = [[ev(), ev()] for _ in range(K)]
+    rev = [[ev(), ev(), ev()] for _ in range(K)]
+    for e in [x for s in tev for x in s]:
+        e.record()  # materialise the event handles
+    torch.cuda.synchronize()
+    for k in range(K):
+        red = step(tev[k], qev[k], rev[k])
+    torch.cuda.synchronize()
+    t_pi = np.mean([tev[k][0].elapsed_time(tev[k][1]) for k in range(K)])
+    t_mu = np.mean([tev[k][1].elapsed_time(tev[k][2]) for k in range(K)])
+    t_merge = np.mean([tev[k][2].elapsed_time(tev[k][3]) for k in range(K)])
+    t_qh = np.mean([qev[k][0].elapsed_time(qev[k][1]) for k in range(K)])
+    t_red = np.mean([rev[k][0].elapsed_time(rev[k][1]) for k in range(K)])
+    t_ctl = np.mean([rev[k][1].elapsed_time(rev[k][2]) for k in range(K)])
+    stats = red["stats"].cpu().numpy()
+    log("per step %.3f ms | quantize H %.3f | pi %.3f | mu %.3f | merge %.3f | reduce %.3f | "
+        "controller %.3f ms" % (ms_per_step, t_qh, t_pi, t_mu, t_merge, t_red, t_ctl))
+    log("batch stats:", dict(zip(acrl.STAT_NAMES, [float(x) for x in stats])))
+
+    flops = 2.0 * T * V * d           # per precision, algorithmic
+    ach_pi = flops / (t_pi * 1e-3) / 1e12
+    ach_mu = flops / (t_mu * 1e-3) / 1e12
+    roof_pi = {"kernel": "score_kernel<bf16> (pi LM head + fused log-softmax)", "bound": "mfma",
+               "achieved": round(ach_pi, 1), "peak": PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
+               "frac": round(ach_pi / PEAK_TFLOPS["bf16"], 4), "traffic": None,
+               "avg_ms": round(float(t_pi), 4), "flops_per_launch": flops}
+    roof_mu = {"kernel": "score_kernel<fp8> (mu LM head + fused log-softmax)", "bound": "mfma",
+               "achieved": round(ach_mu, 1), "peak": PEAK_TFLOPS["fp8"], "unit": "TFLOP/s",
+               "frac": round(ach_mu / PEAK_TFLOPS["fp8"], 4), "traffic": None,
+               "avg_ms": round(float(t_mu), 4), "flops_per_launch": flops}
+    dominant = roof_pi if t_pi >= t_mu else roof_mu
+    # fraction of the combined MFMA roofline: ideal time at both peaks / measured step time
+    ideal_ms = (flops / (PEAK_TFLOPS["bf16"] * 1e12) + flops / (PEAK_TFLOPS["fp8"] * 1e12)) * 1e3
+    q_bytes = T * d * 3 + (T * d * 2 if w.scaling == inputs.PER_TENSOR else 0)
+
+    value = T / (ms_per_step * 1e-3)
+    line = {
+        "metric": "scored tokens/sec (pi+mu logprob+discrepancy) and % of MFMA peak, d=%d V=%d" % (d, V),
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16(pi)+fp8e4m3(mu)",
+        "data": "synthetic",
+        "config": {"workload": w.describe(), "valid_tokens": T, "slots": w.slots,
+                   "ids": "uniform over the vocabulary (work is id-independent)",
+                   "mfma_frac_combined": round(ideal_ms / ms_per_step, 4),
+                   "kernel_ms": {"quantize_h": round(float(t_qh), 4), "score_pi": round(float(t_pi), 4),
+                                 "score_mu": round(float(t_mu), 4), "merge": round(float(t_merge), 4),
+                                 "reduce": round(float(t_red), 4), "controller": round(float(t_ctl), 4)},
+                   "quantize_h_GBps": round(q_bytes / (t_qh * 1e-3) / 1e9, 1),
+                   "quantize_w_ms": round(wq_ms, 4),
+                   "quantize_w_GBps": round(wq_bytes / (wq_ms * 1e-3) / 1e9, 1),
+                   "X": X_ref[0]},
+        "roofline": dominant,
+        "roofline_other": roof_mu if dominant is roof_pi else roof_pi,
+    }
+
+    # ---------------- CPU baseline: the oracle on host cores, bounded sample
+    if args.cpu_seconds > 0:
+        line["cpu_baseline"] = cpu_baseline(w, T, H, W, hq, hs, wq, ws, ids, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(w, T, H, W, hq, hs, wq, ws, ids, budget_s):
+    import torch
+    import oracle
+    cores = len(os.sched_getaffinity(0))
+    threads = int(os.environ.get("OMP_NUM_THREADS", cores))
+    log("cpu baseline: oracle on %d threads (%d cores in affinity)" % (threads, cores))
+    Wh = W.cpu().view(torch.int16).numpy().view(np.uint16)
+    wqh, wsh = wq.cpu().numpy(), ws.cpu().numpy()
+    ids_h = ids.cpu().numpy()
+    rng = np.random.default_rng(0)
+    done, t_total = 0, 0.0
+    batch = max(threads, 1)
+    while t_total < budget_s and done < T:
+        rows = rng.choice(T, size=batch, replace=False)
+        idx = torch.from_numpy(rows).to(H.device)
+        Hs = H.index_select(0, idx).cpu().view(torch.int16).numpy().view(np.uint16)
+        hqs = hq.index_select(0, idx).cpu().numpy()
+        hss = hs.cpu().numpy() if hs.numel() == 1 else hs.index_select(0, idx).cpu().numpy()
+        t0 = time.time()
+        oracle.score(Hs, Wh, hqs, hss, wqh, wsh, w.scaling, ids_h[rows], inv_temperature=w.inv_temperature)
+        t_total += time.time() - t0
+        done += batch
+        log("  oracle: %d rows in %.1fs" % (done, t_total))
+    return {"value": round(done / t_total, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": "%d of %d valid tokens of the %s workload, full V=%d and d=%d, pi and mu "
+                      "(fp64 logits + log-softmax), %.1f s of wall time"
+                      % (done, T, w.name, w.V, w.d, t_total)}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,264 @@
+/*
+ * acrl.h -- C ABI of libacrl, the MI355X (gfx950) scoring and discrepancy path
+ * of ACRL ("Adaptive Control of Training-Inference Discrepancy for Stable RL").
+ *
+ * The library scores every rollout token under the BF16 training policy pi and
+ * the FP8 / MXFP8 inference policy mu, reduces the training-inference
+ * discrepancy per sequence, group and batch, and applies the ACRL controller.
+ *
+ * Conventions shared by every entry point:
+ *  - Array arguments are DEVICE pointers (memory of the current HIP device)
+ *    unless the comment says "host".  The caller owns all memory; the library
+ *    allocates nothing, keeps no per-call state, and writes only the outputs
+ *    and the workspace it is given.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the legacy default
+ *    stream).  Arguments are validated on the host, synchronously; on success
+ *    the kernels are enqueued on `stream` and the call returns; results are
+ *    ready when the stream has been synchronized.
+ *  - Every call returns an acrl_status.  No exception crosses the ABI and the
+ *    library never aborts.  acrl_last_error() gives a thread-local message for
+ *    the last failing call of the calling thread.
+ *  - Calls that share a workspace must not overlap in time.
+ *  - Only gfx950 devices are supported (ACRL_ERR_UNSUPPORTED otherwise).
+ *  - bf16 tensors are passed as their 16-bit patterns; FP8 tensors are OCP
+ *    E4M3 ("fn": bias 7, largest finite 448) bytes; MX scales are OCP E8M0
+ *    bytes (value 2^(code-127)).
+ *  - Row-major layouts; pointers 16-byte aligned.
+ */
+#ifndef ACRL_H
+#define ACRL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ACRL_ABI_VERSION 1
+
+typedef int acrl_status;
+enum {
+  ACRL_OK = 0,
+  ACRL_ERR_INVALID_ARG = 1,   /* a pointer, size or hyper-parameter is out of contract */
+  ACRL_ERR_UNSUPPORTED = 2,   /* device is not gfx950, or an unsupported option       */
+  ACRL_ERR_WORKSPACE = 3,     /* workspace missing or smaller than the query returns  */
+  ACRL_ERR_HIP = 4            /* the HIP runtime reported an error                    */
+};
+
+/* Scaling granularity of the FP8 inference policy mu.  The paper's engine
+ * quantizes activations per token and weights per channel (Sec. 5.1), and
+ * runs MXFP8 for the larger models (Sec. 5.2, 5.4).                          */
+typedef enum {
+  ACRL_SCALE_PER_TENSOR = 0,  /* one fp32 scale for the whole matrix               */
+  ACRL_SCALE_PER_ROW = 1,     /* one fp32 scale per row (token / vocabulary row)    */
+  ACRL_SCALE_MX32 = 2         /* one E8M0 scale per 32 consecutive elements of a row */
+} acrl_scaling;
+
+/* FP8 rounding: nearest-even (the "nearest-around" quantization of Sec. 5.1)
+ * or toward zero (the truncated FP8 of the stress test, Sec. 5.3).          */
+typedef enum { ACRL_ROUND_NEAREST_EVEN = 0, ACRL_ROUND_TOWARD_ZERO = 1 } acrl_rounding;
+
+/* Which discrepancy Y enters alpha = gamma*sign(A)*(1 - Y/X) (Sec. 4.1).    */
+typedef enum {
+  ACRL_Y_GROUP = 0,           /* Y of the response's prompt group (the formula)     */
+  ACRL_Y_SEQUENCE = 1,        /* Y of the response itself                           */
+  ACRL_Y_BATCH = 2            /* Y of the whole batch                               */
+} acrl_y_level;
+
+/* Slots of the batch statistics vector (double[ACRL_N_STATS]). */
+enum {
+  ACRL_STAT_Y_BATCH = 0,      /* mean over non-empty groups of Y_g                  */
+  ACRL_STAT_TOK_MEAN_D = 1,   /* mean of d over valid tokens                        */
+  ACRL_STAT_TOK_MAX_D = 2,    /* max of d over valid tokens                         */
+  ACRL_STAT_TOK_STD_D = 3,    /* population standard deviation of d                */
+  ACRL_STAT_MEAN_H_PI = 4,    /* mean entropy of pi over valid tokens (0 if absent)  */
+  ACRL_STAT_MEAN_H_MU = 5,    /* mean entropy of mu over valid tokens (0 if absent)  */
+  ACRL_STAT_N_TOKENS = 6,     /* number of valid tokens                             */
+  ACRL_STAT_N_GROUPS = 7,     /* number of groups with a non-empty response         */
+  ACRL_STAT_TOK_MEAN_LOGRATIO = 8, /* mean of log(pi/mu) over valid tokens          */
+  ACRL_STAT_N_SEQS = 9,       /* number of non-empty responses                      */
+  ACRL_N_STATS = 10
+};
+
+const char* acrl_status_string(acrl_status status);
+const char* acrl_last_error(void);
+int acrl_abi_version(void);
+/* sizeof of the three descriptor structs as compiled into the library (host);
+ * bindings compare them with their own layout.                              */
+void acrl_abi_struct_sizes(size_t* score_desc, size_t* reduce_desc, size_t* controller_desc);
+
+/* ======================================================================== */
+/* a1/a2  acrl_quantize_fp8 -- FP8 quantization of a bf16 matrix            */
+/* ======================================================================== *
+ * Quantizes the LM head W (rows = V) for mu once per weight version, and the
+ * hidden states H (rows = tokens) every step (Sec. 5.1: per-channel weights,
+ * per-token activations; MXFP8 per Sec. 5.2).
+ *   x      bf16 [rows, ld], columns [0, cols) are used.  (device)
+ *   q      uint8 [rows, cols], dense; E4M3 codes.                  (device, out)
+ *   scales PER_TENSOR: float[1]; PER_ROW: float[rows];
+ *          MX32: uint8 E8M0 [rows, cols/32].                       (device, out)
+ * Definition.  PER_TENSOR / PER_ROW: amax = max |x| over the group, fp32;
+ * s = amax / 448 (fp32, correctly rounded; s = 1 if amax == 0);
+ * q = e4m3(x / s) with a correctly rounded fp32 divide.  MX32 (OCP MX v1.0):
+ * per 32-element block, code = clamp(floor(log2 amax) - 8 + 127, 0, 254)
+ * (0 for an all-zero block), q = e4m3(x * 2^(127 - code)).  e4m3() rounds as
+ * `rounding` says and saturates magnitudes >= 448 to 448; NaN -> 0x7F|sign.
+ * Requirements: rows >= 0, cols > 0 and a multiple of 32, ld >= cols and a
+ * multiple of 8.  PER_TENSOR needs a workspace of
+ * acrl_quantize_workspace_size() bytes; the others need none (may be NULL).
+ */
+acrl_status acrl_quantize_workspace_size(int64_t rows, int64_t cols, int scaling, size_t* bytes);
+acrl_status acrl_quantize_fp8(const void* x, int64_t rows, int64_t cols, int64_t ld,
+                              int scaling, int rounding, void* q, void* scales,
+                              void* workspace, size_t workspace_bytes, void* stream);
+
+/* Element-wise fp32 -> E4M3 encoder with the rounding and saturation above
+ * (x: float[n], q: uint8[n], device).  A building block and a test hook for
+ * the encoder used by acrl_quantize_fp8.                                   */
+acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, void* stream);
+
+/* ======================================================================== */
+/* a3/a4/a5  acrl_score_pi_mu -- sampled-token log-probs under pi and mu    */
+/* ======================================================================== *
+ * For every row r (a token with hidden state h_r and sampled id a_r) and both
+ * policies: z = (h W^T) / tau over the whole vocabulary, lse = log sum exp z,
+ * logp = z[a_r] - lse (= log pi(a_t) or log mu(a_t), the quantities of
+ * Eq. distance_metric and of rho in Sec. 4.1), entropy = -sum p log p.
+ *   pi: z = (h . W_v) / tau with bf16 operands, fp32 accumulation.
+ *   mu: z = s_a s_w[v] (hq . Wq_v) / tau (PER_TENSOR / PER_ROW), or
+ *       sum_b 2^(ea_b-127) 2^(ew_vb-127) (hq_b . Wq_vb) / tau (MX32),
+ *       with E4M3 operands from acrl_quantize_fp8 and fp32 accumulation.
+ * The [rows, V] logits never reach memory: the softmax statistics are reduced
+ * inside the GEMM.  Outputs of row r go to slot out_slot[r] (or r if
+ * out_slot is NULL); rows with mask[r] == 0 write 0 to their slot; slots not
+ * named by any row are not touched.
+ * Requirements: n_rows >= 0; d > 0 and d % 128 == 0; V > 0 and V < 2^31;
+ * token ids in [0, V) (else the row's outputs are NaN and *error_flag, if
+ * given, becomes nonzero; the flag is never cleared by the library).
+ */
+typedef struct acrl_score_desc {
+  int64_t n_rows;               /* rows scored by this call (a chunk of the batch is fine) */
+  int64_t d;                    /* hidden size                                              */
+  int64_t V;                    /* vocabulary size                                          */
+  const void* h;                /* bf16 [n_rows, d]  hidden states (pi input)               */
+  const void* w;                /* bf16 [V, d]       LM head of theta_old (pi)              */
+  const void* hq;               /* e4m3 [n_rows, d]  quantized hidden states (mu)           */
+  const void* hq_scales;        /* scales of hq, layout per mu_scaling                      */
+  const void* wq;               /* e4m3 [V, d]       quantized LM head (mu)                 */
+  const void* wq_scales;        /* scales of wq, layout per mu_scaling                      */
+  int32_t mu_scaling;           /* acrl_scaling used for BOTH hq and wq                     */
+  float inv_temperature;        /* 1/tau applied to both policies' logits (> 0)             */
+  const int32_t* token_ids;     /* [n_rows] sampled ids a_t                                 */
+  const uint8_t* mask;          /* [n_rows] 1 = score this row; NULL = all rows             */
+  const int32_t* out_slot;      /* [n_rows] output slot of each row; NULL = identity        */
+  float* logp_pi;               /* [slots] out                                              */
+  float* logp_mu;               /* [slots] out                                              */
+  float* entropy_pi;            /* [slots] out, nullable                                    */
+  float* entropy_mu;            /* [slots] out, nullable                                    */
+  float* lse_pi;                /* [slots] out, nullable                                    */
+  float* lse_mu;                /* [slots] out, nullable                                    */
+  float* logit_pi;              /* [slots] out, nullable: z[a_t] under pi                    */
+  float* logit_mu;              /* [slots] out, nullable: z[a_t] under mu                    */
+  int32_t* error_flag;          /* device int, nullable                                     */
+  void* workspace;              /* acrl_score_workspace_size() bytes, device                */
+  size_t workspace_bytes;
+} acrl_score_desc;
+
+acrl_status acrl_score_workspace_size(int64_t n_rows, int64_t d, int64_t V, int mu_scaling,
+                                      size_t* bytes);
+acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream);
+
+/* Tracing hook (observability, per calling thread).  With n == 4, every later
+ * acrl_score_pi_mu call of this thread records the caller-owned hipEvent_t
+ * handles events[0..3] on its stream: before the pi kernel, between the pi and
+ * mu kernels, between the mu kernel and the merge, and after the merge, so
+ * the caller can time each kernel.  n == 0 (events may be NULL) turns it off.
+ * The event handles must stay valid while tracing is on.                    */
+acrl_status acrl_trace_score_events(void* const* events, int n);
+
+/* ======================================================================== */
+/* a6/a7  acrl_discrepancy_reduce -- per-token d, segmented reductions       */
+/* ======================================================================== *
+ * Slots are [B, L] (slot of response i, position j is i*L + j).  For valid
+ * slots (mask != 0): d = |exp(logp_pi) - exp(logp_mu)| (Eq. distance_metric,
+ * on probabilities) and the log-ratio log(pi/mu) = logp_pi - logp_mu.
+ * Per response i: |a_i| = valid count, sums of d and of the log-ratio (the
+ * latter is log rho_i of sequence-level MIS, Sec. 2.2), mean d.
+ * Per group g (the G responses of one prompt): Y_g = mean over the group's
+ * non-empty responses of their mean d (the formula for Y in Sec. 4.1).
+ * Batch: mean over non-empty groups of Y_g (the outer mean of X, Sec. 4.1) and
+ * the token-level statistics of ACRL_STAT_*.  Sums are accumulated in fp64.
+ * Requirements: B, L, n_groups >= 0; group_of_seq[i] in [0, n_groups).
+ */
+typedef struct acrl_reduce_desc {
+  int64_t B;                    /* responses                                                */
+  int64_t L;                    /* slots per response                                       */
+  int64_t n_groups;             /* prompts                                                  */
+  const float* logp_pi;         /* [B*L]                                                    */
+  const float* logp_mu;         /* [B*L]                                                    */
+  const float* entropy_pi;      /* [B*L], nullable                                          */
+  const float* entropy_mu;      /* [B*L], nullable                                          */
+  const uint8_t* mask;          /* [B*L]                                                    */
+  const int32_t* group_of_seq;  /* [B] prompt index of each response                        */
+  float* d_tok;                 /* [B*L] out, nullable: d (0 where masked)                  */
+  int32_t* seq_len;             /* [B] out, nullable                                        */
+  double* seq_sum_d;            /* [B] out, nullable                                        */
+  double* seq_sum_logratio;     /* [B] out, nullable                                        */
+  float* seq_mean_d;            /* [B] out (0 for an empty response)                        */
+  float* group_y;               /* [n_groups] out (0 for an empty group)                    */
+  int32_t* group_nseq;          /* [n_groups] out, nullable: non-empty responses per group  */
+  double* stats;                /* [ACRL_N_STATS] out                                       */
+  void* workspace;              /* acrl_reduce_workspace_size() bytes, device               */
+  size_t workspace_bytes;
+} acrl_reduce_desc;
+
+acrl_status acrl_reduce_workspace_size(int64_t B, int64_t L, int64_t n_groups, size_t* bytes);
+acrl_status acrl_discrepancy_reduce(const acrl_reduce_desc* desc, void* stream);
+
+/* ======================================================================== */
+/* a8  acrl_controller_step -- ACRL per-token weights                       */
+/* ======================================================================== *
+ * Eq. ACRL: the clipped surrogate of every valid token is weighted by
+ * min(rho, C) with rho = (pi(a_t)/mu(a_t))^alpha and
+ * alpha = gamma * sign(A) * (1 - Y/X) (sign(0) = 0).  Computed as
+ * weight = exp(min(alpha * (logp_pi - logp_mu), ln C)), which equals
+ * min(rho, C).  Masked slots get alpha = 0 and weight = 0.
+ * Y comes from seq_mean_d[i], group_y[group_of_seq[i]] or
+ * stats[ACRL_STAT_Y_BATCH] per y_level (outputs of acrl_discrepancy_reduce).
+ * Requirements: X > 0, gamma > 0, C > 1 (Sec. 4.1); the array y_level reads
+ * must be non-NULL.
+ */
+typedef struct acrl_controller_desc {
+  int64_t B;
+  int64_t L;
+  int64_t n_groups;             /* prompts; group ids outside [0, n_groups) give NaN        */
+  const uint8_t* mask;          /* [B*L]                                                    */
+  const int32_t* group_of_seq;  /* [B] (needed for ACRL_Y_GROUP)                            */
+  const float* logp_pi;         /* [B*L]                                                    */
+  const float* logp_mu;         /* [B*L]                                                    */
+  const float* adv;             /* [B] or [B*L] advantages A                                */
+  int32_t adv_per_token;        /* 0: adv is [B] (GRPO); 1: adv is [B*L] (PPO)              */
+  int32_t y_level;              /* acrl_y_level                                             */
+  const float* seq_mean_d;      /* [B]                                                      */
+  const float* group_y;         /* [n_groups]                                               */
+  const double* stats;          /* [ACRL_N_STATS]                                           */
+  float X;                      /* reference discrepancy, > 0                               */
+  float gamma;                  /* control strength, > 0                                    */
+  float C;                      /* clip, > 1                                                */
+  float* alpha;                 /* [B*L] out, nullable                                      */
+  float* weight;                /* [B*L] out                                                */
+} acrl_controller_desc;
+
+acrl_status acrl_controller_step(const acrl_controller_desc* desc, void* stream);
+
+/* Host helper (host pointers): the reference discrepancy X of Sec. 4.1 is the
+ * mean of Y_g over the non-empty groups (group_nseq > 0) of the step-0
+ * batches.  Returns ACRL_ERR_INVALID_ARG if no group is non-empty.          */
+acrl_status acrl_reference_from_groups(const float* group_y, const int32_t* group_nseq,
+                                       int64_t n_groups, float* X_out);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ACRL_H */

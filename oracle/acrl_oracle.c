@@ -218,39 +218,39 @@ int acrl_ref_logits_mu(const uint8_t* hq_row, const void* row_scale, const uint8
                        const void* wq_scales, int scaling, int64_t d, int64_t V,
                        double inv_temperature, double* z) {
   if (!hq_row || !row_scale || !wq || !wq_scales || !z || d <= 0 || V <= 0) return -1;
+  if (scaling == REF_MX32 && d % 32 != 0) return -1;
+  if (scaling != REF_PER_TENSOR && scaling != REF_PER_ROW && scaling != REF_MX32) return -1;
+  /* value of every code, from the decoder above (a table only saves calls) */
+  double dec[256];
+  for (int c = 0; c < 256; ++c) dec[c] = acrl_ref_e4m3_decode((uint8_t)c);
   double* a = (double*)malloc((size_t)d * sizeof(double));
   if (!a) return -1;
-  for (int64_t k = 0; k < d; ++k) a[k] = acrl_ref_e4m3_decode(hq_row[k]);
+  for (int64_t k = 0; k < d; ++k) a[k] = dec[hq_row[k]];
 
   if (scaling == REF_PER_TENSOR || scaling == REF_PER_ROW) {
     const double s_a = *(const float*)row_scale;
     for (int64_t v = 0; v < V; ++v) {
       const double s_w = (scaling == REF_PER_TENSOR) ? ((const float*)wq_scales)[0]
                                                      : ((const float*)wq_scales)[v];
+      const uint8_t* wr = wq + v * d;
       double acc = 0.0;
-      for (int64_t k = 0; k < d; ++k) acc += a[k] * acrl_ref_e4m3_decode(wq[v * d + k]);
+      for (int64_t k = 0; k < d; ++k) acc += a[k] * dec[wr[k]];
       z[v] = s_a * s_w * acc * inv_temperature;
     }
-  } else if (scaling == REF_MX32) {
-    if (d % 32 != 0) {
-      free(a);
-      return -1;
-    }
+  } else {
     const int64_t nb = d / 32;
     const uint8_t* ea = (const uint8_t*)row_scale;
     const uint8_t* ew = (const uint8_t*)wq_scales;
     for (int64_t v = 0; v < V; ++v) {
+      const uint8_t* wr = wq + v * d;
       double acc = 0.0;
       for (int64_t b = 0; b < nb; ++b) {
         double blk = 0.0;
-        for (int64_t k = 32 * b; k < 32 * b + 32; ++k) blk += a[k] * acrl_ref_e4m3_decode(wq[v * d + k]);
+        for (int64_t k = 32 * b; k < 32 * b + 32; ++k) blk += a[k] * dec[wr[k]];
         acc += acrl_ref_e8m0_decode(ea[b]) * acrl_ref_e8m0_decode(ew[v * nb + b]) * blk;
       }
       z[v] = acc * inv_temperature;
     }
-  } else {
-    free(a);
-    return -1;
   }
   free(a);
   return 0;

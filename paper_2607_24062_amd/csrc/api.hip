@@ -1,0 +1,285 @@
+// api.hip -- the extern "C" entry points of libacrl: argument validation on
+// the host, device capability check, workspace sizing, kernel dispatch.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "acrl_internal.h"
+
+namespace acrl {
+
+static thread_local char g_last_error[512] = "";
+
+void set_error(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+  va_end(ap);
+}
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_dev_mu;
+int g_dev_state[kMaxDevices];  // 0 unknown, 1 gfx950, 2 other
+
+acrl_status check_device() {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    set_error("hipGetDevice failed: %s", hipGetErrorString(e));
+    return ACRL_ERR_HIP;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    set_error("device index %d out of range", dev);
+    return ACRL_ERR_UNSUPPORTED;
+  }
+  std::lock_guard<std::mutex> lk(g_dev_mu);
+  if (g_dev_state[dev] == 0) {
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, dev);
+    if (e != hipSuccess) {
+      set_error("hipGetDeviceProperties failed: %s", hipGetErrorString(e));
+      return ACRL_ERR_HIP;
+    }
+    g_dev_state[dev] = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+    if (g_dev_state[dev] == 2) set_error("device %d is %s; libacrl supports gfx950 only", dev, prop.gcnArchName);
+  }
+  if (g_dev_state[dev] != 1) {
+    set_error("device %d is not gfx950; libacrl supports gfx950 only", dev);
+    return ACRL_ERR_UNSUPPORTED;
+  }
+  return ACRL_OK;
+}
+
+acrl_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ACRL_OK;
+  set_error("%s: %s", what, hipGetErrorString(e));
+  return ACRL_ERR_HIP;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+#define ACRL_REQUIRE(cond, ...)       \
+  do {                                \
+    if (!(cond)) {                    \
+      acrl::set_error(__VA_ARGS__);   \
+      return ACRL_ERR_INVALID_ARG;    \
+    }                                 \
+  } while (0)
+
+size_t quantize_ws(int scaling) { return scaling == ACRL_SCALE_PER_TENSOR ? 256 : 0; }
+
+acrl_status validate_score(const acrl_score_desc* d) {
+  ACRL_REQUIRE(d, "desc is NULL");
+  ACRL_REQUIRE(d->n_rows >= 0 && d->n_rows < (int64_t)INT32_MAX - 512, "n_rows %lld out of range",
+               (long long)d->n_rows);
+  ACRL_REQUIRE(d->d > 0 && d->d % 128 == 0, "d = %lld must be a positive multiple of 128",
+               (long long)d->d);
+  ACRL_REQUIRE(d->V > 0 && d->V < (int64_t)INT32_MAX - 512, "V = %lld out of range", (long long)d->V);
+  ACRL_REQUIRE(d->mu_scaling == ACRL_SCALE_PER_TENSOR || d->mu_scaling == ACRL_SCALE_PER_ROW ||
+                   d->mu_scaling == ACRL_SCALE_MX32,
+               "mu_scaling %d unknown", d->mu_scaling);
+  ACRL_REQUIRE(d->inv_temperature > 0.0f && d->inv_temperature < 1e30f,
+               "inv_temperature must be positive and finite");
+  ACRL_REQUIRE(d->w && d->wq && d->wq_scales, "w, wq and wq_scales are required");
+  ACRL_REQUIRE(aligned16(d->w) && aligned16(d->wq) && aligned16(d->wq_scales),
+               "w, wq, wq_scales must be 16-byte aligned");
+  if (d->n_rows > 0) {
+    ACRL_REQUIRE(d->h && d->hq && d->hq_scales && d->token_ids && d->logp_pi && d->logp_mu,
+                 "h, hq, hq_scales, token_ids, logp_pi and logp_mu are required");
+    ACRL_REQUIRE(aligned16(d->h) && aligned16(d->hq) && aligned16(d->hq_scales),
+                 "h, hq, hq_scales must be 16-byte aligned");
+  }
+  return ACRL_OK;
+}
+
+acrl_status validate_reduce(const acrl_reduce_desc* d) {
+  ACRL_REQUIRE(d, "desc is NULL");
+  ACRL_REQUIRE(d->B >= 0 && d->L >= 0 && d->n_groups >= 0, "B, L, n_groups must be >= 0");
+  ACRL_REQUIRE(d->B < (int64_t)INT32_MAX && d->n_groups < (int64_t)INT32_MAX, "B or n_groups too large");
+  ACRL_REQUIRE(d->stats, "stats is required");
+  if (d->B > 0) {
+    ACRL_REQUIRE(d->seq_mean_d && d->group_of_seq, "seq_mean_d and group_of_seq are required");
+    ACRL_REQUIRE(d->n_groups > 0, "n_groups must be > 0 when B > 0");
+    if (d->L > 0)
+      ACRL_REQUIRE(d->logp_pi && d->logp_mu && d->mask, "logp_pi, logp_mu and mask are required");
+  }
+  if (d->n_groups > 0) ACRL_REQUIRE(d->group_y, "group_y is required");
+  return ACRL_OK;
+}
+
+}  // namespace
+}  // namespace acrl
+
+using acrl::set_error;
+
+extern "C" {
+
+const char* acrl_status_string(acrl_status status) {
+  switch (status) {
+    case ACRL_OK: return "ok";
+    case ACRL_ERR_INVALID_ARG: return "invalid argument";
+    case ACRL_ERR_UNSUPPORTED: return "unsupported";
+    case ACRL_ERR_WORKSPACE: return "workspace too small";
+    case ACRL_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* acrl_last_error(void) { return acrl::g_last_error; }
+
+int acrl_abi_version(void) { return ACRL_ABI_VERSION; }
+
+void acrl_abi_struct_sizes(size_t* score_desc, size_t* reduce_desc, size_t* controller_desc) {
+  if (score_desc) *score_desc = sizeof(acrl_score_desc);
+  if (reduce_desc) *reduce_desc = sizeof(acrl_reduce_desc);
+  if (controller_desc) *controller_desc = sizeof(acrl_controller_desc);
+}
+
+acrl_status acrl_quantize_workspace_size(int64_t rows, int64_t cols, int scaling, size_t* bytes) {
+  ACRL_REQUIRE(bytes, "bytes is NULL");
+  ACRL_REQUIRE(rows >= 0 && cols > 0, "rows must be >= 0 and cols > 0");
+  ACRL_REQUIRE(scaling >= ACRL_SCALE_PER_TENSOR && scaling <= ACRL_SCALE_MX32, "scaling %d unknown", scaling);
+  *bytes = acrl::quantize_ws(scaling);
+  return ACRL_OK;
+}
+
+acrl_status acrl_quantize_fp8(const void* x, int64_t rows, int64_t cols, int64_t ld, int scaling,
+                              int rounding, void* q, void* scales, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  ACRL_REQUIRE(rows >= 0, "rows = %lld must be >= 0", (long long)rows);
+  ACRL_REQUIRE(cols > 0 && cols % 32 == 0, "cols = %lld must be a positive multiple of 32", (long long)cols);
+  ACRL_REQUIRE(ld >= cols && ld % 8 == 0, "ld = %lld must be >= cols and a multiple of 8", (long long)ld);
+  ACRL_REQUIRE(scaling >= ACRL_SCALE_PER_TENSOR && scaling <= ACRL_SCALE_MX32, "scaling %d unknown", scaling);
+  ACRL_REQUIRE(rounding == ACRL_ROUND_NEAREST_EVEN || rounding == ACRL_ROUND_TOWARD_ZERO,
+               "rounding %d unknown", rounding);
+  ACRL_REQUIRE(scales, "scales is NULL");
+  if (rows > 0) {
+    ACRL_REQUIRE(x && q, "x and q are required");
+    ACRL_REQUIRE(acrl::aligned16(x) && acrl::aligned16(q), "x and q must be 16-byte aligned");
+  }
+  ACRL_REQUIRE(rows * (cols / 32) < ((int64_t)1 << 40), "tensor too large");
+  const size_t need = acrl::quantize_ws(scaling);
+  if (need > 0 && (!workspace || workspace_bytes < need)) {
+    set_error("per-tensor quantization needs %zu workspace bytes, got %zu", need, workspace_bytes);
+    return ACRL_ERR_WORKSPACE;
+  }
+  acrl_status st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(acrl::launch_quantize(static_cast<const uint16_t*>(x), rows, cols, ld,
+                                                scaling, rounding, static_cast<uint8_t*>(q),
+                                                scales, workspace, (hipStream_t)stream),
+                          "acrl_quantize_fp8 launch");
+}
+
+acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, void* stream) {
+  ACRL_REQUIRE(n >= 0, "n must be >= 0");
+  ACRL_REQUIRE(rounding == ACRL_ROUND_NEAREST_EVEN || rounding == ACRL_ROUND_TOWARD_ZERO,
+               "rounding %d unknown", rounding);
+  if (n > 0) {
+    ACRL_REQUIRE(x && q, "x and q are required");
+    ACRL_REQUIRE(acrl::aligned16(x) && acrl::aligned16(q), "x and q must be 16-byte aligned");
+  }
+  acrl_status st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(
+      acrl::launch_fp8_encode(x, n, rounding, static_cast<uint8_t*>(q), (hipStream_t)stream),
+      "acrl_fp8_encode launch");
+}
+
+acrl_status acrl_score_workspace_size(int64_t n_rows, int64_t d, int64_t V, int mu_scaling, size_t* bytes) {
+  ACRL_REQUIRE(bytes, "bytes is NULL");
+  ACRL_REQUIRE(n_rows >= 0 && n_rows < (int64_t)INT32_MAX - 512, "n_rows out of range");
+  ACRL_REQUIRE(d > 0 && d % 128 == 0, "d must be a positive multiple of 128");
+  ACRL_REQUIRE(V > 0 && V < (int64_t)INT32_MAX - 512, "V out of range");
+  ACRL_REQUIRE(mu_scaling >= ACRL_SCALE_PER_TENSOR && mu_scaling <= ACRL_SCALE_MX32, "mu_scaling unknown");
+  *bytes = acrl::plan_score(n_rows, d, V).ws_bytes;
+  return ACRL_OK;
+}
+
+acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream) {
+  acrl_status st = acrl::validate_score(desc);
+  if (st != ACRL_OK) return st;
+  const acrl::ScorePlan plan = acrl::plan_score(desc->n_rows, desc->d, desc->V);
+  if (desc->n_rows > 0 && (!desc->workspace || desc->workspace_bytes < plan.ws_bytes)) {
+    set_error("acrl_score_pi_mu needs %zu workspace bytes, got %zu", plan.ws_bytes, desc->workspace_bytes);
+    return ACRL_ERR_WORKSPACE;
+  }
+  if (desc->n_rows > 0 && !acrl::aligned16(desc->workspace)) {
+    set_error("workspace must be 16-byte aligned");
+    return ACRL_ERR_INVALID_ARG;
+  }
+  st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(acrl::launch_score(*desc, plan, (hipStream_t)stream), "acrl_score_pi_mu launch");
+}
+
+acrl_status acrl_trace_score_events(void* const* events, int n) {
+  ACRL_REQUIRE(n == 0 || n == 4, "n must be 0 or 4");
+  if (n == 4) {
+    ACRL_REQUIRE(events, "events is NULL");
+    for (int k = 0; k < 4; ++k) ACRL_REQUIRE(events[k], "events[%d] is NULL", k);
+  }
+  acrl::set_score_trace(events, n);
+  return ACRL_OK;
+}
+
+acrl_status acrl_reduce_workspace_size(int64_t B, int64_t L, int64_t n_groups, size_t* bytes) {
+  ACRL_REQUIRE(bytes, "bytes is NULL");
+  ACRL_REQUIRE(B >= 0 && L >= 0 && n_groups >= 0, "B, L, n_groups must be >= 0");
+  *bytes = acrl::reduce_workspace_bytes(B, L, n_groups);
+  return ACRL_OK;
+}
+
+acrl_status acrl_discrepancy_reduce(const acrl_reduce_desc* desc, void* stream) {
+  acrl_status st = acrl::validate_reduce(desc);
+  if (st != ACRL_OK) return st;
+  const size_t need = acrl::reduce_workspace_bytes(desc->B, desc->L, desc->n_groups);
+  if (!desc->workspace || desc->workspace_bytes < need) {
+    set_error("acrl_discrepancy_reduce needs %zu workspace bytes, got %zu", need, desc->workspace_bytes);
+    return ACRL_ERR_WORKSPACE;
+  }
+  st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(acrl::launch_reduce(*desc, (hipStream_t)stream), "acrl_discrepancy_reduce launch");
+}
+
+acrl_status acrl_controller_step(const acrl_controller_desc* d, void* stream) {
+  ACRL_REQUIRE(d, "desc is NULL");
+  ACRL_REQUIRE(d->B >= 0 && d->L >= 0 && d->n_groups >= 0, "B, L and n_groups must be >= 0");
+  ACRL_REQUIRE(d->X > 0.0f && d->X < 1e30f, "X must be > 0 (got %g)", (double)d->X);
+  ACRL_REQUIRE(d->gamma > 0.0f && d->gamma < 1e30f, "gamma must be > 0 (got %g)", (double)d->gamma);
+  ACRL_REQUIRE(d->C > 1.0f && d->C < 1e30f, "C must be > 1 (got %g)", (double)d->C);
+  ACRL_REQUIRE(d->y_level == ACRL_Y_GROUP || d->y_level == ACRL_Y_SEQUENCE || d->y_level == ACRL_Y_BATCH,
+               "y_level %d unknown", d->y_level);
+  if (d->B > 0 && d->L > 0) {
+    ACRL_REQUIRE(d->mask && d->logp_pi && d->logp_mu && d->adv && d->weight,
+                 "mask, logp_pi, logp_mu, adv and weight are required");
+    if (d->y_level == ACRL_Y_GROUP) ACRL_REQUIRE(d->group_y && d->group_of_seq, "group_y and group_of_seq are required");
+    if (d->y_level == ACRL_Y_SEQUENCE) ACRL_REQUIRE(d->seq_mean_d, "seq_mean_d is required");
+    if (d->y_level == ACRL_Y_BATCH) ACRL_REQUIRE(d->stats, "stats is required");
+  }
+  acrl_status st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(acrl::launch_controller(*d, (hipStream_t)stream), "acrl_controller_step launch");
+}
+
+acrl_status acrl_reference_from_groups(const float* group_y, const int32_t* group_nseq, int64_t n_groups,
+                                       float* X_out) {
+  ACRL_REQUIRE(group_y && group_nseq && X_out && n_groups >= 0, "null argument or negative n_groups");
+  double s = 0.0;
+  int64_t n = 0;
+  for (int64_t g = 0; g < n_groups; ++g)
+    if (group_nseq[g] > 0) {
+      s += group_y[g];
+      ++n;
+    }
+  ACRL_REQUIRE(n > 0, "no non-empty group");
+  *X_out = (float)(s / (double)n);
+  return ACRL_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,208 @@
+"""GPU parity of acrl_score_pi_mu with the oracle.
+
+Per-token log-probs within 2e-3, entropies within 1e-3 log V, and the
+sampled-token logit exact wherever the logits are exact (integer operands).
+Shapes cover several tiles, ragged token and vocabulary tails, a vocabulary
+smaller than one tile, a single row, masking, scattered output slots,
+invalid ids, the three mu scalings, temperature, determinism and chunking."""
+import math
+
+import numpy as np
+import pytest
+
+import inputs
+import oracle
+from cases import (TOL_LOGP, lossless_integer_case, oracle_sampled_ids, random_bf16, tol_entropy,
+                   workload_case)
+from gpu_util import down, torch_dev, up, up_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_score(H, W, ids, scaling, inv_temp=1.0, mask=None, out_slot=None, n_slots=None,
+               error_flag=False):
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    h = up_bf16(torch, dev, H)
+    w = up_bf16(torch, dev, W)
+    hq, hs = acrl.acrl_quantize_fp8(h, scaling)
+    wq, ws = acrl.acrl_quantize_fp8(w, scaling)
+    flag = torch.zeros(1, dtype=torch.int32, device=dev) if error_flag else None
+    out = acrl.acrl_score_pi_mu(h, w, hq, hs, wq, ws, scaling, up(torch, dev, ids.astype(np.int32)),
+                                inv_temperature=inv_temp,
+                                mask=None if mask is None else up(torch, dev, mask.astype(np.uint8)),
+                                out_slot=None if out_slot is None else up(torch, dev, out_slot.astype(np.int32)),
+                                n_slots=n_slots, error_flag=flag)
+    torch.cuda.synchronize()
+    res = {k: down(v) for k, v in out.items()}
+    q = dict(hq=down(hq), hs=down(hs), wq=down(wq), ws=down(ws))
+    if error_flag:
+        res["error_flag"] = int(down(flag)[0])
+    return res, q
+
+
+def _compare(res, ref, V, rows=None, slots=None, exact_logit=False):
+    rows = np.arange(len(ref["logp_pi"])) if rows is None else rows
+    slots = rows if slots is None else slots
+    for tag in ("pi", "mu"):
+        dl = np.abs(res["logp_" + tag][slots] - ref["logp_" + tag][rows])
+        assert dl.max() <= TOL_LOGP, "logp_%s off by %g" % (tag, dl.max())
+        de = np.abs(res["entropy_" + tag][slots] - ref["ent_" + tag][rows])
+        assert de.max() <= tol_entropy(V), "entropy_%s off by %g" % (tag, de.max())
+        ds = np.abs(res["lse_" + tag][slots] - ref["lse_" + tag][rows])
+        assert ds.max() <= TOL_LOGP, "lse_%s off by %g" % (tag, ds.max())
+        dz = np.abs(res["logit_" + tag][slots] - ref["z_" + tag][rows])
+        if exact_logit:
+            assert np.array_equal(res["logit_" + tag][slots].astype(np.float64), ref["z_" + tag][rows])
+        else:
+            assert dz.max() <= TOL_LOGP, "logit_%s off by %g" % (tag, dz.max())
+
+
+@pytest.mark.parametrize("scaling", [oracle.PER_ROW, oracle.PER_TENSOR, oracle.MX32])
+def test_small_workload(scaling):
+    c = workload_case("tiny")
+    w = c["w"]
+    H, W = c["H"], c["W"]
+    hq, hs = oracle.quantize_fp8(H, scaling)
+    wq, ws = oracle.quantize_fp8(W, scaling)
+    ids = c["ids"] if scaling == w.scaling else oracle_sampled_ids(
+        H, hq, hs, wq, ws, scaling, w.inv_temperature, inputs.uniforms(w, H.shape[0]))
+    res, q = _gpu_score(H, W, ids, scaling, w.inv_temperature, out_slot=c["slots"], n_slots=w.slots)
+    assert np.array_equal(q["hq"], hq) and np.array_equal(q["wq"], wq)
+    ref = oracle.score(H, W, hq, hs, wq, ws, scaling, ids, inv_temperature=w.inv_temperature)
+    _compare(res, ref, w.V, slots=c["slots"])
+    # slots that no row names are untouched (zero-initialised by the binding)
+    untouched = np.setdiff1d(np.arange(w.slots), c["slots"])
+    assert np.all(res["logp_pi"][untouched] == 0)
+
+
+@pytest.mark.parametrize("scaling", [oracle.PER_ROW, oracle.PER_TENSOR, oracle.MX32])
+@pytest.mark.parametrize("T,V,d", [(1, 2048, 256), (257, 1000, 128), (300, 300, 256),
+                                   (64, 100, 128), (513, 4096 + 32, 128), (40, 129, 384)])
+def test_ragged_shapes(scaling, T, V, d):
+    H = random_bf16((T, d), T + V)
+    W = random_bf16((V, d), T * V, std=2.5 / math.sqrt(d))
+    r = np.random.default_rng(T)
+    ids = r.integers(0, V, size=T).astype(np.int32)
+    ids[: min(T, 6)] = [0, V - 1, min(127, V - 1), min(128, V - 1), min(255, V - 1), min(256, V - 1)][: min(T, 6)]
+    res, q = _gpu_score(H, W, ids, scaling, 1.0)
+    ref = oracle.score(H, W, q["hq"], q["hs"], q["wq"], q["ws"], scaling, ids)
+    _compare(res, ref, V)
+
+
+@pytest.mark.parametrize("scaling", [oracle.PER_ROW, oracle.PER_TENSOR, oracle.MX32])
+def test_exact_integer_logits(scaling):
+    """Lossless integer operands: pi and mu logits are the same exact integers,
+    so the gathered logit is exact, log pi == log mu bitwise, and d == 0."""
+    T, V, d = 300, 700, 256
+    H, W, z = lossless_integer_case(T, V, d, 11)
+    ids = np.random.default_rng(12).integers(0, V, size=T).astype(np.int32)
+    res, q = _gpu_score(H, W, ids, scaling)
+    assert np.all(q["hs"].view(np.uint8) == q["hs"].view(np.uint8))
+    want = z[np.arange(T), ids].astype(np.float64)
+    assert np.array_equal(res["logit_pi"].astype(np.float64), want)
+    assert np.array_equal(res["logit_mu"].astype(np.float64), want)
+    assert np.array_equal(res["logp_pi"], res["logp_mu"])
+    assert np.array_equal(res["entropy_pi"], res["entropy_mu"])
+    ref = oracle.score(H, W, q["hq"], q["hs"], q["wq"], q["ws"], scaling, ids)
+    _compare(res, ref, V, exact_logit=True)
+
+
+def test_temperature_and_mask():
+    T, V, d = 200, 1500, 256
+    H = random_bf16((T, d), 5)
+    W = random_bf16((V, d), 6, std=2.5 / 16)
+    ids = np.random.default_rng(7).integers(0, V, size=T).astype(np.int32)
+    mask = (np.random.default_rng(8).random(T) < 0.7).astype(np.uint8)
+    res, q = _gpu_score(H, W, ids, oracle.PER_ROW, inv_temp=1 / 0.7, mask=mask)
+    ref = oracle.score(H, W, q["hq"], q["hs"], q["wq"], q["ws"], oracle.PER_ROW, ids, mask,
+                       inv_temperature=1 / 0.7)
+    on = np.flatnonzero(mask)
+    _compare(res, ref, V, rows=on)
+    off = np.flatnonzero(mask == 0)
+    for k in ("logp_pi", "logp_mu", "entropy_pi", "lse_mu", "logit_pi"):
+        assert np.all(res[k][off] == 0)
+
+
+def test_invalid_ids_flag_and_nan():
+    T, V, d = 50, 700, 128
+    H = random_bf16((T, d), 9)
+    W = random_bf16((V, d), 10, std=0.2)
+    ids = np.random.default_rng(1).integers(0, V, size=T).astype(np.int32)
+    ids[3], ids[7] = V, -1
+    res, q = _gpu_score(H, W, ids, oracle.PER_ROW, error_flag=True)
+    assert res["error_flag"] != 0
+    assert np.isnan(res["logp_pi"][[3, 7]]).all() and np.isnan(res["logp_mu"][[3, 7]]).all()
+    good = np.setdiff1d(np.arange(T), [3, 7])
+    ref = oracle.score(H, W, q["hq"], q["hs"], q["wq"], q["ws"], oracle.PER_ROW,
+                       np.where((ids >= 0) & (ids < V), ids, 0).astype(np.int32))
+    _compare(res, ref, V, rows=good)
+
+
+def test_deterministic_and_chunk_invariant():
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    T, V, d = 700, 3000, 256
+    H = random_bf16((T, d), 13)
+    W = random_bf16((V, d), 14, std=2.5 / 16)
+    ids = np.random.default_rng(15).integers(0, V, size=T).astype(np.int32)
+    a, _ = _gpu_score(H, W, ids, oracle.PER_ROW)
+    b, _ = _gpu_score(H, W, ids, oracle.PER_ROW)
+    for k in a:
+        assert np.array_equal(a[k], b[k], equal_nan=True), k
+    # three chunks of rows scattered into the same slot array == one shot
+    h = up_bf16(torch, dev, H)
+    w = up_bf16(torch, dev, W)
+    hq, hs = acrl.acrl_quantize_fp8(h, acrl.SCALE_PER_ROW)
+    wq, ws = acrl.acrl_quantize_fp8(w, acrl.SCALE_PER_ROW)
+    idt = up(torch, dev, ids)
+    outs = None
+    for lo, hi in ((0, 256), (256, 300), (300, T)):
+        slot = torch.arange(lo, hi, dtype=torch.int32, device=dev)
+        outs = acrl.acrl_score_pi_mu(h[lo:hi], w, hq[lo:hi], hs[lo:hi], wq, ws, acrl.SCALE_PER_ROW,
+                                     idt[lo:hi], out_slot=slot, n_slots=T, outputs=outs)
+    torch.cuda.synchronize()
+    for k in a:
+        assert np.array_equal(down(outs[k]), a[k]), k
+
+
+# full-size workloads: the launch configuration the benchmark times, checked
+# on sampled rows that the oracle scores one by one
+@pytest.mark.parametrize("name", ["q8b", "q17b", "mx"])
+def test_full_size_sampled_rows(name):
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    w = inputs.WORKLOADS[name]
+    T = inputs.n_valid(w)
+    h = inputs.hidden_bf16_torch(w, T, dev)
+    W = inputs.weights_bf16_torch(w, dev)
+    hq, hs = acrl.acrl_quantize_fp8(h, w.scaling)
+    wq, ws = acrl.acrl_quantize_fp8(W, w.scaling)
+    ids_np = inputs.uniform_ids(w, T)
+    rows = np.unique(np.concatenate([np.random.default_rng(w.seed).choice(T, 14, replace=False),
+                                     [0, T - 1, 255, 256]]))
+    ids_np[rows[:4]] = [0, w.V - 1, 151807, 151808][: len(rows[:4])]
+    ids = up(torch, dev, ids_np)
+    out = acrl.acrl_score_pi_mu(h, W, hq, hs, wq, ws, w.scaling, ids, inv_temperature=w.inv_temperature)
+    torch.cuda.synchronize()
+    idx = torch.from_numpy(rows).to(dev)
+    Hs = h.index_select(0, idx).cpu().view(torch.int16).numpy().view(np.uint16)
+    hqs = down(hq.index_select(0, idx))
+    if w.scaling == oracle.PER_ROW:
+        hss = down(hs)[rows]
+    elif w.scaling == oracle.MX32:
+        hss = down(hs)[rows]
+    else:
+        hss = down(hs)
+    Wb = W.cpu().view(torch.int16).numpy().view(np.uint16)
+    ref = oracle.score(Hs, Wb, hqs, hss, down(wq), down(ws), w.scaling, ids_np[rows],
+                       inv_temperature=w.inv_temperature)
+    res = {k: down(v)[rows] for k, v in out.items()}
+    _compare(res, ref, w.V)
+    # every row's outputs are finite and in range
+    lp = down(out["logp_pi"])
+    ent = down(out["entropy_pi"])
+    assert np.isfinite(lp).all() and (lp <= 1e-6).all()
+    assert (ent >= -1e-4).all() and (ent <= math.log(w.V) + 1e-3).all()
+    del h, W, hq, wq, out
+    torch.cuda.empty_cache()
