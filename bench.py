@@ -182,7 +182,7 @@ def main():
 
     value = T / (ms_per_step * 1e-3)
     line = {
-        "metric": "scored tokens/sec (pi+mu logprob+discrepancy) and % of MFMA peak, d=%d V=%d" % (d, V),
+        "metric": "scored tokens/sec (pi+mu logprob+discrepancy) and %% of MFMA peak, d=%d V=%d" % (d, V),
         "value": round(value, 1),
         "unit": "tokens/s",
         "n_gpus": 1,

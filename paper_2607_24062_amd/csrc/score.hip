@@ -183,30 +183,34 @@ void score_kernel(ScoreParams p) {
       load16_to_lds(gb + ((uint32_t)row * rb + (uint32_t)lcol), lb + k * 8 * kChunk);
     }
     if constexpr (MODE == kMX) {
-      // the two E8M0 scales (K blocks 4kc+2g, 4kc+2g+1) this lane's fragments
-      // use in the chunk's two MFMA steps
+      // the four E8M0 scales of the chunk's MX blocks for this lane's row
       const uint32_t mrb = (uint32_t)p.mx_row_bytes;
       const int sa_first = v0 + wv * 128, sb_first = t0 + wt * 128;
       const int sa_base = min(sa_first, p.V - 1), sb_base = min(sb_first, p.n_rows - 1);
-      const uint8_t* sa = p.a_mx + (int64_t)sa_base * p.mx_row_bytes + kc * 4 + 2 * g;
-      const uint8_t* sb = p.b_mx + (int64_t)sb_base * p.mx_row_bytes + kc * 4 + 2 * g;
+      const uint8_t* sa = p.a_mx + (int64_t)sa_base * p.mx_row_bytes + kc * 4;
+      const uint8_t* sb = p.b_mx + (int64_t)sb_base * p.mx_row_bytes + kc * 4;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
         const int row = min(sa_first + b * 32 + r32, p.V - 1) - sa_base;
-        mxa_next[b] = *reinterpret_cast<const uint16_t*>(sa + (uint32_t)row * mrb);
+        mxa_next[b] = *reinterpret_cast<const uint32_t*>(sa + (uint32_t)row * mrb);
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int row = min(sb_first + j * 32 + r32, p.n_rows - 1) - sb_base;
-        mxb_next[j] = *reinterpret_cast<const uint16_t*>(sb + (uint32_t)row * mrb);
+        mxb_next[j] = *reinterpret_cast<const uint32_t*>(sb + (uint32_t)row * mrb);
       }
     }
   };
 
-  // K permutation inside a 128-byte chunk: lane group g supplies bytes
-  // [64g, 64g+64) of its row; step s of the chunk takes the s-th piece of it.
-  // A (W rows) and B (H rows) use the same permutation, so the dot products
-  // are unchanged; for MX every 32-byte piece is exactly one scale block.
+  // K permutation inside a 128-byte chunk.  BF16 (4 MFMA steps of K=16):
+  // lane group g supplies bytes [64g, 64g+64) of its row, step s the s-th
+  // 16-byte piece.  FP8 (2 steps of K=64): an f8f6f4 operand is two 16-byte
+  // halves per lane, and the MFMA treats register half h of BOTH lane groups
+  // as its K block h (whose E8M0 scale lanes 32h..32h+31 supply).  Step s
+  // therefore feeds half h with MX block 2s+h of the chunk: lane group g
+  // takes its 16-byte piece g, i.e. 16-byte column 2(2s+h)+g of the row.
+  // A (W rows) and B (H rows) use the same permutation, so dot products are
+  // unchanged, and each MX block keeps its own scale.
   auto compute = [&](int stage) {
     const uint8_t* As = lds + stage * kStageBytes + (wv * 128 + r32) * kChunk;
     const uint8_t* Bs = lds + stage * kStageBytes + (kTileV + wt * 128 + r32) * kChunk;
@@ -228,8 +232,8 @@ void score_kernel(ScoreParams p) {
     } else {
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
-        const int off0 = ((4 * g + 2 * s) ^ sw) << 4;
-        const int off1 = ((4 * g + 2 * s + 1) ^ sw) << 4;
+        const int off0 = ((4 * s + g) ^ sw) << 4;      // register half 0: block 2s
+        const int off1 = ((4 * s + 2 + g) ^ sw) << 4;  // register half 1: block 2s+1
         i32x8 bv[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -245,8 +249,9 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
           for (int j = 0; j < 4; ++j) {
             if constexpr (MODE == kMX) {
-              const int sa = (mxa[b] >> (8 * s)) & 0xFF;
-              const int sb = (mxb[j] >> (8 * s)) & 0xFF;
+              // lane group g supplies the scale of K block g of this step
+              const int sa = (mxa[b] >> (8 * (2 * s + g))) & 0xFF;
+              const int sb = (mxb[j] >> (8 * (2 * s + g))) & 0xFF;
               acc[b][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bv[j], acc[b][j],
                                                                          0, 0, 0, sa, 0, sb);
             } else {
