@@ -26,6 +26,10 @@ struct ScorePlan {
   int n_vtiles;         // vocabulary tiles of 256 rows
   int tiles_per_strip;  // vocabulary tiles per workgroup
   int n_strips;         // vocabulary strips (partial softmax states per row)
+  int n_tblocks;        // token-tile blocks of kBlockT tiles (grid rasterization)
+  int n_sblocks;        // strip blocks of kBlockS strips
+  int n_blocks_pad;     // n_tblocks * n_sblocks rounded up to a multiple of 8
+  int grid;             // workgroups launched (n_blocks_pad * kBlockT * kBlockS)
   size_t ws_part_offset[2];  // byte offsets of the (M, S, U) partials of pi / mu
   size_t ws_logit_offset[2]; // byte offsets of the sampled-token logits of pi / mu
   size_t ws_bytes;

@@ -23,6 +23,8 @@
 //    lse = ln2 (M + log2 S), entropy = ln2 (log2 S - U/S).
 //  * The strip's state per token goes to a workspace (split-V partials); a
 //    merge kernel combines the strips and writes logp = z[a_t] - lse.
+#include <type_traits>
+
 #include "acrl_internal.h"
 
 namespace acrl {
@@ -31,15 +33,24 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x8 __attribute__((ext_vector_type(8)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 enum ScoreMode { kBF16 = 0, kFP8Tensor = 1, kFP8Row = 2, kMX = 3 };
 
 constexpr int kTileV = 256;            // vocabulary rows per workgroup tile
 constexpr int kTileT = 256;            // tokens per workgroup tile
-constexpr int kChunk = 128;            // bytes of K per row per pipeline stage
+constexpr int kChunk = 64;             // bytes of K per row per pipeline stage
 constexpr int kThreads = 256;
-constexpr int kStageBytes = (kTileV + kTileT) * kChunk;  // 64 KiB
+constexpr int kStageBytes = (kTileV + kTileT) * kChunk;  // 32 KiB
 constexpr float kInitMax = -1.0e30f;   // running max before any logit was seen
+// Grid rasterization: the 32 workgroups an XCD runs at the same time (one per
+// CU) form a block of kBlockT token tiles x kBlockS vocabulary strips, so
+// each H chunk is shared by 8 and each W chunk by 4 workgroups in that
+// XCD's L2.  Workgroups are dispatched to the 8 XCDs round-robin.
+constexpr int kXcds = 8;
+constexpr int kBlockT = 4;
+constexpr int kBlockS = 8;
 
 struct ScoreParams {
   const uint8_t* a;        // W (bf16) or Wq (e4m3): [V, row_bytes]
@@ -51,6 +62,8 @@ struct ScoreParams {
   int n_vtiles;
   int tiles_per_strip;
   int n_strips;
+  int n_ttiles;
+  int n_tblocks;
   const float* a_scale;    // FP8 per-row: [V]; per-tensor: [1]
   const float* b_scale;    // FP8 per-row: [n_rows]; per-tensor: [1]
   const uint8_t* a_mx;     // MX: E8M0 [V, d/32]
@@ -80,44 +93,83 @@ __device__ __forceinline__ void merge_state(float& M, float& S, float& U, float 
   M = Mn;
 }
 
-// 16 bytes per lane from global memory straight into LDS: lane l of the wave
-// writes lds_wave_base + 16*l (gfx950 global_load_lds_dwordx4).
-__device__ __forceinline__ void load16_to_lds(const void* gsrc, uint8_t* lds_wave_base) {
-  __builtin_amdgcn_global_load_lds(
-      (const void __attribute__((address_space(1)))*)gsrc,
-      (void __attribute__((address_space(3)))*)lds_wave_base, 16, 0, 0);
+// Buffer resource of `bytes` bytes at `base` (raw, unswizzled; gfx9 dword 3).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-__device__ __forceinline__ void wait_vm_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-// acc[b][j][i] with 16b + i == idx, as an exact one-hot weighted sum: the
-// weights max(1 - |idx - k|, 0) are exactly 0 or 1, so no lane masks or
-// dynamically indexed registers are needed.
-__device__ __forceinline__ float pick64(const f32x16 (&a)[4][4], int j, int idx) {
-  float fi = (float)idx;
-  // keep the weight arithmetic inside the (rarely taken) branch of the caller
-  asm volatile("v_mov_b32 %0, %0" : "+v"(fi));
-  float z = 0.0f;
-#pragma unroll
-  for (int b = 0; b < 4; ++b)
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      z = fmaf(fmaxf(1.0f - fabsf(fi - (float)(16 * b + i)), 0.0f), a[b][j][i], z);
-  return z;
+// SIZE (4 or 16) bytes per lane from a buffer straight into LDS: lane l of
+// the wave writes lds_wave_base + SIZE*l (buffer_load ... lds).  voffset is
+// the lane's byte offset, soffset a wave-uniform byte offset.
+template <int SIZE>
+__device__ __forceinline__ void buffer_to_lds(__amdgpu_buffer_rsrc_t r, uint32_t voffset, uint32_t soffset,
+                                              uint8_t* lds_wave_base) {
+  auto* l = (__attribute__((address_space(3))) void*)lds_wave_base;
+  if constexpr (SIZE == 16) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, l, 16, (int)voffset, (int)soffset, 0, 0);
+  else if constexpr (SIZE == 4) __builtin_amdgcn_raw_ptr_buffer_load_lds(r, l, 4, (int)voffset, (int)soffset, 0, 0);
+  else static_assert(SIZE == 16, "size must be 4 or 16");
 }
+
+// One accumulator value, read out of its AGPR exactly here (an opaque read:
+// the compiler may neither hoist it nor keep a VGPR copy of the whole tile).
+__device__ __forceinline__ float acc_read(float a) {
+  float r;
+  asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(r) : "a"(a));
+  return r;
+}
+
+
+// Wait until at most N vector-memory loads of this wave are outstanding
+// (gfx9 s_waitcnt encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt
+// left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+// Operand stages in LDS (one 64-byte K chunk of every row of both tiles per
+// stage).  MX also streams a small stage of E8M0 scales per chunk, and the
+// per-row FP8 mode keeps the weight-row scales of the last NS + 1 vocabulary
+// tiles (a tile's scales arrive with its first chunk, up to NS chunks before
+// the previous tile's epilogue reads its own), so both keep one operand
+// stage less.
+template <int MODE>
+struct Pipe {
+  static constexpr int kStages = (MODE == kMX || MODE == kFP8Row) ? 4 : 5;
+  static constexpr int kScaleBytes = (MODE == kMX) ? (kTileV + kTileT) * 4 : 0;  // per stage
+  static constexpr int kRowScaleSlots = kStages + 1;
+  static constexpr int kRowScaleBytes = (MODE == kFP8Row) ? kRowScaleSlots * kTileV * 4 : 0;
+  static constexpr int kLoadsPerChunk = (MODE == kMX) ? 10 : 8;  // per wave, at least
+};
 
 template <int MODE>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void score_kernel(ScoreParams p) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStageBytes];
+  constexpr int NS = Pipe<MODE>::kStages;
+  constexpr int SB = Pipe<MODE>::kScaleBytes;
+  constexpr int LPC = Pipe<MODE>::kLoadsPerChunk;
+  constexpr int RSB = Pipe<MODE>::kRowScaleBytes;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[NS * (kStageBytes + SB) + RSB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wv = wave & 1;   // which 128-row half of the vocabulary tile
   const int wt = wave >> 1;  // which 128-token half of the token tile
-  const int r32 = lane & 31, g = lane >> 5, sw = lane & 7;
+  const int r32 = lane & 31, g = lane >> 5;
+  const int sw = (lane >> 2) & 3;  // swizzle of this lane's fragment row (see below)
 
-  const int st = blockIdx.x % p.n_strips;
-  const int t0 = (blockIdx.x / p.n_strips) * kTileT;
+  // ---- which (token tile, strip) this workgroup owns
+  int tt, st;
+  {
+    const int xcd = blockIdx.x % kXcds, i = blockIdx.x / kXcds;
+    const int per = kBlockT * kBlockS;
+    const int blk = (i / per) * kXcds + xcd;  // blocks in dispatch order, 8 at a time
+    const int k = i % per;
+    tt = (blk % p.n_tblocks) * kBlockT + k / kBlockS;
+    st = (blk / p.n_tblocks) * kBlockS + k % kBlockS;
+  }
+  if (tt >= p.n_ttiles || st >= p.n_strips) return;  // padding of the grid
+  const int t0 = tt * kTileT;
   const int vt_begin = st * p.tiles_per_strip;
   const int vt_end = min(vt_begin + p.tiles_per_strip, p.n_vtiles);
   const int n_iter = (vt_end - vt_begin) * p.n_chunks;
@@ -147,134 +199,156 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
 
-  // ---- global -> LDS: wave w moves rows [64w, 64w+64) of both operand
-  // tiles, 8 rows (1 KiB) per instruction.  Lane l fills LDS slot l of the
-  // 1 KiB block: row 8k + l/8, swizzled column l%8, i.e. logical column
-  // (l%8) ^ (row%8) of that row.
-  const int lrow = lane >> 3;                     // row within the 8-row block
-  const int lcol = ((lane & 7) ^ lrow) << 4;      // byte offset of the logical column
-  uint32_t mxa_next[4], mxb_next[4], mxa[4], mxb[4];
+  // ---- global -> LDS.  A stage holds one 64-byte K chunk of all 256 + 256
+  // rows (W tile rows first).  A row's 16-byte column c sits at position
+  // c ^ ((row/4) % 4): the 16 lanes one LDS cycle serves read 16 consecutive
+  // rows and hit 16 distinct bank groups.  Wave w moves rows [64w, 64w+64)
+  // of each tile, 16 rows (1 KiB) per instruction; lane l fills slot l of
+  // the 1 KiB block: row 16k + l/4, position l%4, so it loads logical column
+  // (l%4) ^ ((l/16)%4) of that row.  Loads are buffer loads from a resource
+  // spanning the tile's rows: 32-bit lane offsets, the chunk's K offset in
+  // the scalar offset.  Rows past the end of W / H are clamped to its last
+  // row.
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const int lrow = lane >> 2;
+  const uint32_t lcol = (uint32_t)(((lane & 3) ^ ((lane >> 4) & 3)) << 4);
+  const uint32_t rb = (uint32_t)p.row_bytes;
+  const int b_rows = min(kTileT, p.n_rows - t0);  // valid rows of the token tile
+  const __amdgpu_buffer_rsrc_t rsrc_b = make_rsrc(p.b + (int64_t)t0 * p.row_bytes, (uint32_t)b_rows * rb);
+  uint32_t off_b[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) off_b[k] = (uint32_t)min(wave_u * 64 + 16 * k + lrow, b_rows - 1) * rb + lcol;
+  auto stage_at = [&](int stg) { return lds + stg * kStageBytes; };
+  auto scales_at = [&](int stg) { return lds + NS * kStageBytes + stg * SB; };
+  auto rowscales_at = [&](int q) {  // FP8 per-row: weight-row scales of tile q
+    return reinterpret_cast<float*>(lds + NS * (kStageBytes + SB) + (q % Pipe<MODE>::kRowScaleSlots) * kTileV * 4);
+  };
 
-  // Row offsets are 32-bit and relative to a wave-uniform base row, so the
-  // loads take the scalar-base + vector-offset form.  Rows past the end of W
-  // (or of H) are clamped to its last row; the base row is clamped too, so
-  // every offset is in [0, 64).
-  const int b_first = t0 + wave * 64;
-  const int b_base = min(b_first, p.n_rows - 1);
-  auto issue_loads = [&](int it, int stage) {
-    const int q = it / p.n_chunks;
-    const int kc = it - q * p.n_chunks;
+  auto issue_chunk = [&](int c, int stg) {
+    const int q = c / p.n_chunks;
+    const int kc = c - q * p.n_chunks;
     const int v0 = (vt_begin + q) * kTileV;
-    const int a_first = v0 + wave * 64;
-    const int a_base = min(a_first, p.V - 1);
-    const uint8_t* ga = p.a + (int64_t)a_base * p.row_bytes + (int64_t)kc * kChunk;
-    const uint8_t* gb = p.b + (int64_t)b_base * p.row_bytes + (int64_t)kc * kChunk;
-    const uint32_t rb = (uint32_t)p.row_bytes;
-    uint8_t* la = lds + stage * kStageBytes + (wave * 64) * kChunk;
+    const int a_rows = min(kTileV, p.V - v0);  // valid rows of the vocabulary tile
+    const __amdgpu_buffer_rsrc_t rsrc_a = make_rsrc(p.a + (int64_t)v0 * p.row_bytes, (uint32_t)a_rows * rb);
+    const uint32_t koff = (uint32_t)kc * kChunk;
+    uint8_t* la = stage_at(stg) + (wave_u * 64) * kChunk;
     uint8_t* lb = la + kTileV * kChunk;
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int row = min(a_first + 8 * k + lrow, p.V - 1) - a_base;
-      load16_to_lds(ga + ((uint32_t)row * rb + (uint32_t)lcol), la + k * 8 * kChunk);
+    for (int k = 0; k < 4; ++k) {
+      const uint32_t off = (uint32_t)min(wave_u * 64 + 16 * k + lrow, a_rows - 1) * rb + lcol;
+      buffer_to_lds<16>(rsrc_a, off, koff, la + k * 16 * kChunk);
     }
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int row = min(b_first + 8 * k + lrow, p.n_rows - 1) - b_base;
-      load16_to_lds(gb + ((uint32_t)row * rb + (uint32_t)lcol), lb + k * 8 * kChunk);
+    for (int k = 0; k < 4; ++k) buffer_to_lds<16>(rsrc_b, off_b[k], koff, lb + k * 16 * kChunk);
+    if constexpr (MODE == kFP8Row) {
+      // with a tile's first chunk: its 256 weight-row scales (lane l of wave
+      // w moves row 64w + l); they land long before the tile's epilogue
+      if (kc == 0) {
+        const __amdgpu_buffer_rsrc_t rs = make_rsrc(p.a_scale + v0, (uint32_t)a_rows * 4);
+        buffer_to_lds<4>(rs, (uint32_t)min(wave_u * 64 + lane, a_rows - 1) * 4, 0,
+                         reinterpret_cast<uint8_t*>(rowscales_at(q)) + wave_u * 64 * 4);
+      }
     }
     if constexpr (MODE == kMX) {
-      // the four E8M0 scales of the chunk's MX blocks for this lane's row
+      // the E8M0 scales of MX blocks 2kc, 2kc+1 of each row: the aligned
+      // dword holding them (blocks 4(kc/2) .. 4(kc/2)+3; rows hold d/32 scale
+      // bytes, a multiple of 4), one dword per row, lane l of wave w moving
+      // row 64w + l of each tile.  The chunk's two bytes sit at byte
+      // 2 (kc % 2) of the dword.
       const uint32_t mrb = (uint32_t)p.mx_row_bytes;
-      const int sa_first = v0 + wv * 128, sb_first = t0 + wt * 128;
-      const int sa_base = min(sa_first, p.V - 1), sb_base = min(sb_first, p.n_rows - 1);
-      const uint8_t* sa = p.a_mx + (int64_t)sa_base * p.mx_row_bytes + kc * 4;
-      const uint8_t* sb = p.b_mx + (int64_t)sb_base * p.mx_row_bytes + kc * 4;
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int row = min(sa_first + b * 32 + r32, p.V - 1) - sa_base;
-        mxa_next[b] = *reinterpret_cast<const uint32_t*>(sa + (uint32_t)row * mrb);
-      }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int row = min(sb_first + j * 32 + r32, p.n_rows - 1) - sb_base;
-        mxb_next[j] = *reinterpret_cast<const uint32_t*>(sb + (uint32_t)row * mrb);
-      }
+      const __amdgpu_buffer_rsrc_t sa = make_rsrc(p.a_mx + (int64_t)v0 * p.mx_row_bytes, (uint32_t)a_rows * mrb);
+      const __amdgpu_buffer_rsrc_t sb = make_rsrc(p.b_mx + (int64_t)t0 * p.mx_row_bytes, (uint32_t)b_rows * mrb);
+      const uint32_t soff = (uint32_t)(kc >> 1) * 4;
+      buffer_to_lds<4>(sa, (uint32_t)min(wave_u * 64 + lane, a_rows - 1) * mrb, soff,
+                       scales_at(stg) + wave_u * 64 * 4);
+      buffer_to_lds<4>(sb, (uint32_t)min(wave_u * 64 + lane, b_rows - 1) * mrb, soff,
+                       scales_at(stg) + (kTileV + wave_u * 64) * 4);
     }
   };
 
-  // K permutation inside a 128-byte chunk.  BF16 (4 MFMA steps of K=16):
-  // lane group g supplies bytes [64g, 64g+64) of its row, step s the s-th
-  // 16-byte piece.  FP8 (2 steps of K=64): an f8f6f4 operand is two 16-byte
-  // halves per lane, and the MFMA treats register half h of BOTH lane groups
-  // as its K block h (whose E8M0 scale lanes 32h..32h+31 supply).  Step s
-  // therefore feeds half h with MX block 2s+h of the chunk: lane group g
-  // takes its 16-byte piece g, i.e. 16-byte column 2(2s+h)+g of the row.
-  // A (W rows) and B (H rows) use the same permutation, so dot products are
-  // unchanged, and each MX block keeps its own scale.
-  auto compute = [&](int stage) {
-    const uint8_t* As = lds + stage * kStageBytes + (wv * 128 + r32) * kChunk;
-    const uint8_t* Bs = lds + stage * kStageBytes + (kTileV + wt * 128 + r32) * kChunk;
+  // ---- MFMA fragments.  K permutation inside a chunk (the same for W and
+  // H rows, so dot products are unchanged).  BF16 (2 MFMA steps of K=16):
+  // lane group g of step s supplies 16-byte column 2s+g of its row.  FP8
+  // (1 step of K=64): an f8f6f4 operand is two 16-byte halves per lane, and
+  // the MFMA treats register half h of BOTH lane groups as its K block h,
+  // whose E8M0 scale the lanes of group h supply; half h therefore holds MX
+  // block h of the chunk, lane group g its 16-byte piece g (column 2h+g).
+  // A group = one (step, vocabulary block b): 4 MFMAs sharing the A fragment.
+  constexpr int G = (MODE == kBF16) ? 8 : 4;  // groups per chunk
+  using FragT = typename std::conditional<MODE == kBF16, bf16x8, i32x8>::type;
+  auto frag_off = [&](int grp) {  // byte offset of the fragment's first 16-byte piece in its row
+    if constexpr (MODE == kBF16) return ((2 * (grp >> 2) + g) ^ sw) << 4;
+    else return (g ^ sw) << 4;
+  };
+  // LDS reads use typed vector loads: the compiler then trusts them not to
+  // alias the LDS written by the buffer -> LDS loads and adds no vmcnt wait of
+  // its own before them (such a wait would drain the whole pipeline).  The
+  // order of DMA and reads comes from the explicit vmcnt waits and barriers.
+  auto read16x2 = [&](const uint8_t* row) -> FragT {
     if constexpr (MODE == kBF16) {
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int off = ((4 * g + s) ^ sw) << 4;
-        bf16x8 bv[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) bv[j] = *reinterpret_cast<const bf16x8*>(Bs + j * 32 * kChunk + off);
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const bf16x8 af = *reinterpret_cast<const bf16x8*>(As + b * 32 * kChunk + off);
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[b][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af, bv[j], acc[b][j], 0, 0, 0);
-        }
-      }
+      return *reinterpret_cast<const bf16x8*>(row);
     } else {
+      const int off0 = (g ^ sw) << 4, off1 = ((2 + g) ^ sw) << 4;
+      const i32x4 x0 = *reinterpret_cast<const i32x4*>(row + off0);
+      const i32x4 x1 = *reinterpret_cast<const i32x4*>(row + off1);
+      return __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7);
+    }
+  };
+  // A fragment of group grp (vocabulary block grp%4), B fragments of its step
+  auto read_a = [&](int stg, int grp) -> FragT {
+    const uint8_t* row = stage_at(stg) + (wv * 128 + (grp & 3) * 32 + r32) * kChunk;
+    if constexpr (MODE == kBF16) return read16x2(row + frag_off(grp));
+    else return read16x2(row);
+  };
+  auto read_b = [&](int stg, int grp, FragT (&bf)[4]) {
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const int off0 = ((4 * s + g) ^ sw) << 4;      // register half 0: block 2s
-        const int off1 = ((4 * s + 2 + g) ^ sw) << 4;  // register half 1: block 2s+1
-        i32x8 bv[4];
+    for (int j = 0; j < 4; ++j) {
+      const uint8_t* row = stage_at(stg) + (kTileV + wt * 128 + j * 32 + r32) * kChunk;
+      if constexpr (MODE == kBF16) bf[j] = read16x2(row + frag_off(grp));
+      else bf[j] = read16x2(row);
+    }
+  };
+  // MX scales of the chunk in stage stg: every tile has an even number of
+  // chunks (d is a multiple of 128) and NS is even, so the chunk's position
+  // in its tile has the parity of stg; lane group g takes block 2kc + g.
+  static_assert(MODE != kMX || NS % 2 == 0, "MX scale parity needs an even stage count");
+  auto read_sa = [&](int stg, int grp) -> int {
+    return scales_at(stg)[(wv * 128 + (grp & 3) * 32 + r32) * 4 + (stg & 1) * 2 + g];
+  };
+  auto read_sb = [&](int stg, int (&sb)[4]) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint4 x0 = *reinterpret_cast<const uint4*>(Bs + j * 32 * kChunk + off0);
-          const uint4 x1 = *reinterpret_cast<const uint4*>(Bs + j * 32 * kChunk + off1);
-          bv[j] = i32x8{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w, (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
-        }
+    for (int j = 0; j < 4; ++j) sb[j] = scales_at(stg)[(kTileV + wt * 128 + j * 32 + r32) * 4 + (stg & 1) * 2 + g];
+  };
+  auto mfma_group = [&](int grp, const FragT& fa, const FragT (&fb)[4], int sa, const int (&sb)[4]) {
+    const int bb = grp & 3;
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const uint4 x0 = *reinterpret_cast<const uint4*>(As + b * 32 * kChunk + off0);
-          const uint4 x1 = *reinterpret_cast<const uint4*>(As + b * 32 * kChunk + off1);
-          const i32x8 af = i32x8{(int)x0.x, (int)x0.y, (int)x0.z, (int)x0.w, (int)x1.x, (int)x1.y, (int)x1.z, (int)x1.w};
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if constexpr (MODE == kMX) {
-              // lane group g supplies the scale of K block g of this step
-              const int sa = (mxa[b] >> (8 * (2 * s + g))) & 0xFF;
-              const int sb = (mxb[j] >> (8 * (2 * s + g))) & 0xFF;
-              acc[b][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bv[j], acc[b][j],
-                                                                         0, 0, 0, sa, 0, sb);
-            } else {
-              acc[b][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bv[j], acc[b][j],
-                                                                         0, 0, 0, 0, 0, 0);
-            }
-          }
-        }
+    for (int j = 0; j < 4; ++j) {
+      if constexpr (MODE == kBF16) {
+        acc[bb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb[j], acc[bb][j], 0, 0, 0);
+      } else if constexpr (MODE == kMX) {
+        acc[bb][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], acc[bb][j], 0, 0, 0,
+                                                                    sa, 0, sb[j]);
+      } else {
+        (void)sa;
+        (void)sb;
+        acc[bb][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], acc[bb][j], 0, 0, 0,
+                                                                    0, 0, 0);
       }
     }
   };
 
-  // Fold one finished vocabulary tile into the running per-token states.
-  // acc[b][j][i] is the logit (before scaling) of vocabulary row
-  // v0 + 32b + 8(i/4) + 4g + (i%4) and token tok[j].
   // Fold one finished vocabulary tile into the running per-token states.
   // acc[b][j][i] is the logit (before scaling) of vocabulary row
   // v0 + 32b + 8(i/4) + 4g + (i%4) and token tok[j]; the 64 rows a lane holds
-  // increase with 16b + i.  Rows past V were loaded as copies of row V-1, so
-  // they hold a genuine logit: they may enter the max, and only their
-  // contributions to S and U are removed, by the weight min(max(nv - idx, 0), 1)
-  // where nv is the number of valid rows of the lane (a prefix of its rows).
-  auto epilogue = [&](int tile) {
+  // increase with 16b + i.  Online softmax at the granularity of these
+  // 16-value blocks: each block is read once, its maximum re-bases the
+  // running state, then its exponentials, sums and (rarely) the sampled
+  // logit come from the same 16 registers.  Rows past V were loaded as
+  // copies of row V-1, so they hold a genuine logit: they may enter the
+  // maximum, and only their contributions to S and U are removed, by the
+  // weight min(max(nv - idx, 0), 1) with nv the lane's count of valid rows
+  // (a prefix of its rows).
+  auto epilogue = [&](int tile, int q) {
     const int v0 = tile * kTileV + wv * 128;
     const bool partial = v0 + 128 > p.V;
     float nv = 64.0f;
@@ -285,96 +359,139 @@ void score_kernel(ScoreParams p) {
       for (int k = 0; k < 16; ++k) n += min(max(lim - 8 * k, 0), 4);
       nv = (float)n;
     }
-    if constexpr (MODE == kFP8Row) {
-      // multiply in the per-row weight scales, four consecutive rows at a time
+    // keep the 64 tail weights derived from nv inside the epilogue (else they
+    // are computed before the K loop and held across it)
+    asm volatile("v_mov_b32 %0, %0" : "+v"(nv));
 #pragma unroll
-      for (int b = 0; b < 4; ++b)
+    for (int b = 0; b < 4; ++b) {
+      float rs[16];
+      if constexpr (MODE == kFP8Row) {
+        const float* rsl = rowscales_at(q) + wv * 128 + b * 32 + 4 * g;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int r0 = v0 + b * 32 + 8 * q + 4 * g;
-          float f[4];
-          if (!partial) {
-            const float4 v = *reinterpret_cast<const float4*>(p.a_scale + r0);
-            f[0] = v.x; f[1] = v.y; f[2] = v.z; f[3] = v.w;
-          } else {
-#pragma unroll
-            for (int k = 0; k < 4; ++k) f[k] = p.a_scale[min(r0 + k, p.V - 1)];
-          }
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-#pragma unroll
-            for (int k = 0; k < 4; ++k) acc[b][j][4 * q + k] *= f[k];
-          __builtin_amdgcn_sched_barrier(0);
+        for (int qq = 0; qq < 4; ++qq) {
+          const f32x4 f = *reinterpret_cast<const f32x4*>(rsl + 8 * qq);
+          rs[4 * qq + 0] = f[0]; rs[4 * qq + 1] = f[1]; rs[4 * qq + 2] = f[2]; rs[4 * qq + 3] = f[3];
         }
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      float mraw = -INFINITY;
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mraw = fmaxf(mraw, acc[b][j][i]);
-        __builtin_amdgcn_sched_barrier(0);
       }
-      const float Mn = fmaxf(M[j], mraw * c2[j]);
-      const float dM = M[j] - Mn;
-      const float al = fast_exp2(dM);
-      U[j] = al * fmaf(dM, S[j], U[j]);
-      S[j] *= al;
-      M[j] = Mn;
-      const float nM = -Mn;
-      float s0 = 0.f, u0 = 0.f;
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
+      for (int j = 0; j < 4; ++j) {
+        float v[16];
+        float m = -INFINITY;
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
-          const float t = fmaf(acc[b][j][i], c2[j], nM);
+          v[i] = acc_read(acc[b][j][i]);
+          if constexpr (MODE == kFP8Row) v[i] *= rs[i];
+          m = fmaxf(m, v[i]);
+        }
+        const float Mn = fmaxf(M[j], m * c2[j]);
+        const float dM = M[j] - Mn;
+        const float al = fast_exp2(dM);
+        U[j] = al * fmaf(dM, S[j], U[j]);
+        S[j] *= al;
+        M[j] = Mn;
+        const float nM = -Mn;
+        float s0 = 0.f, u0 = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float t = fmaf(v[i], c2[j], nM);
           float e = fast_exp2(t);
           if (partial) e *= fminf(fmaxf(nv - (float)(16 * b + i), 0.0f), 1.0f);
           s0 += e;
           u0 = fmaf(e, t, u0);
         }
+        S[j] += s0;
+        U[j] += u0;
+        // finish the update here, ahead of the branch below: otherwise the
+        // pass is sunk past it and the values of all 16 blocks stay live
+        asm volatile("" : "+v"(M[j]), "+v"(S[j]), "+v"(U[j]));
+        // the sampled token a_t: rare branch, taken by the one lane holding it
+        const int rel = id[j] - v0;
+        if ((unsigned)rel < 128u && (rel >> 5) == b && ((rel >> 2) & 1) == g) {
+          float fi = (float)(((rel & 31) >> 3) * 4 + (rel & 3));
+          asm volatile("v_mov_b32 %0, %0" : "+v"(fi));  // keep the weights inside the branch
+          float z = 0.0f;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) z = fmaf(fmaxf(1.0f - fabsf(fi - (float)i), 0.0f), v[i], z);
+          if (tok[j] < p.n_rows && id[j] < p.V) p.logit[tok[j]] = z * cz[j];
+        }
         __builtin_amdgcn_sched_barrier(0);
       }
-      S[j] += s0;
-      U[j] += u0;
-      // the sampled token a_t: rare branch, taken by the one lane holding it
-      const int rel = id[j] - v0;
-      if ((unsigned)rel < 128u && ((rel >> 2) & 1) == g) {
-        const int idx = (rel >> 5) * 16 + ((rel & 31) >> 3) * 4 + (rel & 3);
-        const float z = pick64(acc, j, idx) * cz[j];
-        if (tok[j] < p.n_rows && id[j] < p.V) p.logit[tok[j]] = z;
-      }
-      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
-  issue_loads(0, 0);
-  if constexpr (MODE == kMX) {
+  // ---- the pipeline.  Chunks 0..NS-1 are requested up front, one per
+  // stage.  At the end of chunk c (between its last two MFMA groups) every
+  // wave waits for its part of chunk c+1, the workgroup meets at the one
+  // barrier of the chunk, chunk c+NS is requested into c's stage (no wave
+  // reads it any more), and the first fragments of chunk c+1 are read while
+  // the last MFMA group of chunk c runs.
 #pragma unroll
-    for (int k = 0; k < 4; ++k) { mxa[k] = mxa_next[k]; mxb[k] = mxb_next[k]; }
-  }
-  wait_vm_all();
+  for (int c = 0; c < NS; ++c)
+    if (c < n_iter) issue_chunk(c, c);
+  if (n_iter < NS) wait_vmcnt<0>();
+  else wait_vmcnt<(NS - 1) * LPC>();
   __syncthreads();
+  FragT a_cur, a_nxt, b_cur[4], b_nxt[4];
+  int sa_cur = 0, sa_nxt = 0, sb_cur[4] = {0, 0, 0, 0}, sb_nxt[4] = {0, 0, 0, 0};
+  a_cur = read_a(0, 0);
+  read_b(0, 0, b_cur);
+  if constexpr (MODE == kMX) {
+    sa_cur = read_sa(0, 0);
+    read_sb(0, sb_cur);
+  }
+  a_nxt = a_cur;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) b_nxt[j] = b_cur[j];
+
   int it = 0;
   for (int q = 0; q < vt_end - vt_begin; ++q) {
-#pragma unroll
-    for (int b = 0; b < 4; ++b)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
     for (int kc = 0; kc < p.n_chunks; ++kc, ++it) {
-      const int stage = it & 1;
-      if (it + 1 < n_iter) issue_loads(it + 1, stage ^ 1);  // lands in the other stage
-      compute(stage);
-      if constexpr (MODE == kMX) {
+      const int stg = it % NS;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) { mxa[k] = mxa_next[k]; mxb[k] = mxb_next[k]; }
+      for (int grp = 0; grp < G; ++grp) {
+        const bool new_step = grp + 1 < G && ((grp + 1) & 3) == 0;  // BF16: second K step
+        if (grp + 1 < G) {
+          a_nxt = read_a(stg, grp + 1);
+          if constexpr (MODE == kMX) sa_nxt = read_sa(stg, grp + 1);
+          if (new_step) read_b(stg, grp + 1, b_nxt);
+        } else if (it + 1 < n_iter) {
+          // chunk it+1 must have landed; chunks it+2 .. it+NS-1 may be in flight
+          const int ahead = min(NS - 2, n_iter - 2 - it);
+          if (ahead >= NS - 2) wait_vmcnt<(NS - 2) * LPC>();
+          else if (ahead == 2) wait_vmcnt<2 * LPC>();
+          else if (ahead == 1) wait_vmcnt<LPC>();
+          else wait_vmcnt<0>();
+          __syncthreads();
+          if (it + NS < n_iter) issue_chunk(it + NS, stg);
+          const int nst = (it + 1) % NS;
+          a_nxt = read_a(nst, 0);
+          read_b(nst, 0, b_nxt);
+          if constexpr (MODE == kMX) {
+            sa_nxt = read_sa(nst, 0);
+            read_sb(nst, sb_nxt);
+          }
+        }
+        mfma_group(grp, a_cur, b_cur, sa_cur, sb_cur);
+        a_cur = a_nxt;
+        sa_cur = sa_nxt;
+        if (new_step || grp + 1 == G) {
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            b_cur[j] = b_nxt[j];
+            sb_cur[j] = sb_nxt[j];
+          }
+        }
       }
-      wait_vm_all();
-      __syncthreads();
+      if (kc == p.n_chunks - 1) {
+        epilogue(vt_begin + q, q);
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
+      }
     }
-    epilogue(vt_begin + q);
   }
+  __syncthreads();  // every wave is done with the stages before LDS is reused
 
   // ---- merge the lane pair (l, l^32), then the two vocabulary halves
 #pragma unroll
@@ -478,24 +595,35 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V) {
   ScorePlan pl{};
   pl.n_ttiles = (int)((n_rows + kTileT - 1) / kTileT);
   pl.n_vtiles = (int)((V + kTileV - 1) / kTileV);
-  // Choose the number of vocabulary strips: one workgroup per CU (256 CUs),
-  // minimise the makespan ceil(WGs/256) * tiles-per-WG; ties -> fewer strips.
+  pl.n_tblocks = (pl.n_ttiles + kBlockT - 1) / kBlockT;
+  // Strips: a multiple of kBlockS (or every tile its own strip when there
+  // are fewer tiles).  One workgroup per CU (256 CUs): minimise the makespan
+  // ceil(grid / 256) * (tiles-per-strip + 1/2), the half tile standing for a
+  // workgroup's fixed cost (prologue, state merge, partial writes); ties ->
+  // fewer strips.
   const int64_t cus = 256;
-  int best_s = 1;
+  int best_s = 0;
   int64_t best_cost = -1;
-  for (int s = 1; s <= pl.n_vtiles; ++s) {
-    const int64_t tps = (pl.n_vtiles + s - 1) / s;
-    const int64_t strips = (pl.n_vtiles + tps - 1) / tps;
-    if (strips != s) continue;  // same as a smaller s
-    const int64_t wgs = (int64_t)pl.n_ttiles * s;
-    const int64_t cost = ((wgs + cus - 1) / cus) * tps;
+  auto consider = [&](int s) {
+    const int tps = (pl.n_vtiles + s - 1) / s;
+    const int strips = (pl.n_vtiles + tps - 1) / tps;
+    const int sblocks = (strips + kBlockS - 1) / kBlockS;
+    int blocks = pl.n_tblocks * sblocks;
+    blocks = (blocks + kXcds - 1) / kXcds * kXcds;
+    const int64_t grid = (int64_t)blocks * kBlockT * kBlockS;
+    const int64_t cost = ((grid + cus - 1) / cus) * (2 * tps + 1);
     if (best_cost < 0 || cost < best_cost) {
       best_cost = cost;
-      best_s = s;
+      best_s = strips;
     }
-  }
+  };
+  if (pl.n_vtiles <= kBlockS) consider(pl.n_vtiles);
+  for (int s = kBlockS; s <= pl.n_vtiles; s += kBlockS) consider(s);
   pl.tiles_per_strip = (pl.n_vtiles + best_s - 1) / best_s;
   pl.n_strips = (pl.n_vtiles + pl.tiles_per_strip - 1) / pl.tiles_per_strip;
+  pl.n_sblocks = (pl.n_strips + kBlockS - 1) / kBlockS;
+  pl.n_blocks_pad = (pl.n_tblocks * pl.n_sblocks + kXcds - 1) / kXcds * kXcds;
+  pl.grid = pl.n_blocks_pad * kBlockT * kBlockS;
   const size_t part_bytes = align_up((size_t)3 * pl.n_strips * (size_t)n_rows * sizeof(float), 256);
   const size_t logit_bytes = align_up((size_t)n_rows * sizeof(float), 256);
   size_t off = 0;
@@ -514,7 +642,7 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V) {
 hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStream_t s) {
   if (dsc.n_rows == 0) return hipSuccess;
   uint8_t* ws = static_cast<uint8_t*>(dsc.workspace);
-  const unsigned grid = (unsigned)((int64_t)pl.n_ttiles * pl.n_strips);
+  const unsigned grid = (unsigned)pl.grid;
 
   ScoreParams pp{};
   pp.V = (int)dsc.V;
@@ -522,6 +650,8 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   pp.n_vtiles = pl.n_vtiles;
   pp.tiles_per_strip = pl.tiles_per_strip;
   pp.n_strips = pl.n_strips;
+  pp.n_ttiles = pl.n_ttiles;
+  pp.n_tblocks = pl.n_tblocks;
   pp.inv_temp = dsc.inv_temperature;
   pp.ids = dsc.token_ids;
   pp.mx_row_bytes = (int)(dsc.d / 32);
