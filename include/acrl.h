@@ -134,8 +134,11 @@ acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, vo
  * out_slot is NULL); rows with mask[r] == 0 write 0 to their slot; slots not
  * named by any row are not touched.
  * Requirements: n_rows >= 0; d > 0 and d % 128 == 0; V > 0 and V < 2^31;
+ * for rows = V and rows = n_rows: (rows rounded up to 256) * d / 8 < 2^32;
  * token ids in [0, V) (else the row's outputs are NaN and *error_flag, if
  * given, becomes nonzero; the flag is never cleared by the library).
+ * The workspace holds a tiled copy of W, h, Wq and hq (about 3 (V + n_rows) d
+ * bytes) besides the per-strip partial states.
  */
 typedef struct acrl_score_desc {
   int64_t n_rows;               /* rows scored by this call (a chunk of the batch is fine) */

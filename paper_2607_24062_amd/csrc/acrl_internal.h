@@ -32,6 +32,7 @@ struct ScorePlan {
   int grid;             // workgroups launched (n_blocks_pad * kBlockT * kBlockS)
   size_t ws_part_offset[2];  // byte offsets of the (M, S, U) partials of pi / mu
   size_t ws_logit_offset[2]; // byte offsets of the sampled-token logits of pi / mu
+  size_t ws_pack_offset[4];  // byte offsets of the packed W, H (bf16) and Wq, Hq (e4m3)
   size_t ws_bytes;
 };
 ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V);

@@ -72,6 +72,13 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 size_t quantize_ws(int scaling) { return scaling == ACRL_SCALE_PER_TENSOR ? 256 : 0; }
 
+// The packed operand images are addressed in 16-byte units with 32-bit
+// indices: (rows rounded up to 256) * 2d / 16 must stay below 2^32.
+bool score_size_ok(int64_t rows, int64_t d) {
+  const int64_t padded = (rows + 255) / 256 * 256;
+  return padded * (d / 8) < ((int64_t)1 << 32);
+}
+
 acrl_status validate_score(const acrl_score_desc* d) {
   ACRL_REQUIRE(d, "desc is NULL");
   ACRL_REQUIRE(d->n_rows >= 0 && d->n_rows < (int64_t)INT32_MAX - 512, "n_rows %lld out of range",
@@ -79,6 +86,8 @@ acrl_status validate_score(const acrl_score_desc* d) {
   ACRL_REQUIRE(d->d > 0 && d->d % 128 == 0, "d = %lld must be a positive multiple of 128",
                (long long)d->d);
   ACRL_REQUIRE(d->V > 0 && d->V < (int64_t)INT32_MAX - 512, "V = %lld out of range", (long long)d->V);
+  ACRL_REQUIRE(score_size_ok(d->V, d->d) && score_size_ok(d->n_rows, d->d),
+               "rows x d too large (rows rounded up to 256, times d/8, must be below 2^32)");
   ACRL_REQUIRE(d->mu_scaling == ACRL_SCALE_PER_TENSOR || d->mu_scaling == ACRL_SCALE_PER_ROW ||
                    d->mu_scaling == ACRL_SCALE_MX32,
                "mu_scaling %d unknown", d->mu_scaling);
@@ -196,6 +205,7 @@ acrl_status acrl_score_workspace_size(int64_t n_rows, int64_t d, int64_t V, int 
   ACRL_REQUIRE(d > 0 && d % 128 == 0, "d must be a positive multiple of 128");
   ACRL_REQUIRE(V > 0 && V < (int64_t)INT32_MAX - 512, "V out of range");
   ACRL_REQUIRE(mu_scaling >= ACRL_SCALE_PER_TENSOR && mu_scaling <= ACRL_SCALE_MX32, "mu_scaling unknown");
+  ACRL_REQUIRE(acrl::score_size_ok(V, d) && acrl::score_size_ok(n_rows, d), "rows x d too large");
   *bytes = acrl::plan_score(n_rows, d, V).ws_bytes;
   return ACRL_OK;
 }

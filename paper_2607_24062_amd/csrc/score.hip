@@ -23,6 +23,7 @@
 //    lse = ln2 (M + log2 S), entropy = ln2 (log2 S - U/S).
 //  * The strip's state per token goes to a workspace (split-V partials); a
 //    merge kernel combines the strips and writes logp = z[a_t] - lse.
+#include <algorithm>
 #include <type_traits>
 
 #include "acrl_internal.h"
@@ -43,6 +44,7 @@ constexpr int kTileT = 256;            // tokens per workgroup tile
 constexpr int kChunk = 64;             // bytes of K per row per pipeline stage
 constexpr int kThreads = 256;
 constexpr int kStageBytes = (kTileV + kTileT) * kChunk;  // 32 KiB
+constexpr int kPackBlock = kTileV * kChunk;               // packed image of one (tile, chunk): 16 KiB
 constexpr float kInitMax = -1.0e30f;   // running max before any logit was seen
 // Grid rasterization: the 32 workgroups an XCD runs at the same time (one per
 // CU) form a block of kBlockT token tiles x kBlockS vocabulary strips, so
@@ -53,10 +55,9 @@ constexpr int kBlockT = 4;
 constexpr int kBlockS = 8;
 
 struct ScoreParams {
-  const uint8_t* a;        // W (bf16) or Wq (e4m3): [V, row_bytes]
-  const uint8_t* b;        // H or Hq: [n_rows, row_bytes]
-  int64_t row_bytes;
-  int n_chunks;            // row_bytes / kChunk
+  const uint8_t* a;        // packed W (bf16) or Wq (e4m3): [n_vtiles][n_chunks][16 KiB]
+  const uint8_t* b;        // packed H or Hq: [n_ttiles][n_chunks][16 KiB]
+  int n_chunks;            // bytes per row / kChunk
   int V;
   int n_rows;
   int n_vtiles;
@@ -200,24 +201,19 @@ void score_kernel(ScoreParams p) {
     for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
 
   // ---- global -> LDS.  A stage holds one 64-byte K chunk of all 256 + 256
-  // rows (W tile rows first).  A row's 16-byte column c sits at position
-  // c ^ ((row/4) % 4): the 16 lanes one LDS cycle serves read 16 consecutive
-  // rows and hit 16 distinct bank groups.  Wave w moves rows [64w, 64w+64)
-  // of each tile, 16 rows (1 KiB) per instruction; lane l fills slot l of
-  // the 1 KiB block: row 16k + l/4, position l%4, so it loads logical column
-  // (l%4) ^ ((l/16)%4) of that row.  Loads are buffer loads from a resource
-  // spanning the tile's rows: 32-bit lane offsets, the chunk's K offset in
-  // the scalar offset.  Rows past the end of W / H are clamped to its last
-  // row.
+  // rows (W tile rows first).  Operands come packed (pack_kernel): the
+  // 16 KiB image of each (256-row tile, chunk) pair is stored contiguously
+  // exactly as the stage holds it, so a wave moves 4 KiB of contiguous
+  // memory per tile with 4 buffer -> LDS loads of 1 KiB (lane l: bytes
+  // [16l, 16l+16) of the KiB).  In the image a row's 16-byte column c sits at
+  // position c ^ ((row/4) % 4): the 16 lanes one LDS cycle serves read 16
+  // consecutive rows and hit 16 distinct bank groups.  Rows past the end of
+  // W / H hold copies of its last row.
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  const int lrow = lane >> 2;
-  const uint32_t lcol = (uint32_t)(((lane & 3) ^ ((lane >> 4) & 3)) << 4);
-  const uint32_t rb = (uint32_t)p.row_bytes;
+  const uint32_t lane_off = (uint32_t)lane * 16;
+  const uint32_t tile_bytes = (uint32_t)p.n_chunks * kPackBlock;  // packed bytes of one tile
   const int b_rows = min(kTileT, p.n_rows - t0);  // valid rows of the token tile
-  const __amdgpu_buffer_rsrc_t rsrc_b = make_rsrc(p.b + (int64_t)t0 * p.row_bytes, (uint32_t)b_rows * rb);
-  uint32_t off_b[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) off_b[k] = (uint32_t)min(wave_u * 64 + 16 * k + lrow, b_rows - 1) * rb + lcol;
+  const __amdgpu_buffer_rsrc_t rsrc_b = make_rsrc(p.b + (int64_t)tt * tile_bytes, tile_bytes);
   auto stage_at = [&](int stg) { return lds + stg * kStageBytes; };
   auto scales_at = [&](int stg) { return lds + NS * kStageBytes + stg * SB; };
   auto rowscales_at = [&](int q) {  // FP8 per-row: weight-row scales of tile q
@@ -229,17 +225,14 @@ void score_kernel(ScoreParams p) {
     const int kc = c - q * p.n_chunks;
     const int v0 = (vt_begin + q) * kTileV;
     const int a_rows = min(kTileV, p.V - v0);  // valid rows of the vocabulary tile
-    const __amdgpu_buffer_rsrc_t rsrc_a = make_rsrc(p.a + (int64_t)v0 * p.row_bytes, (uint32_t)a_rows * rb);
-    const uint32_t koff = (uint32_t)kc * kChunk;
-    uint8_t* la = stage_at(stg) + (wave_u * 64) * kChunk;
+    const __amdgpu_buffer_rsrc_t rsrc_a = make_rsrc(p.a + (int64_t)(vt_begin + q) * tile_bytes, tile_bytes);
+    const uint32_t soff = (uint32_t)kc * kPackBlock + (uint32_t)wave_u * 4096;
+    uint8_t* la = stage_at(stg) + wave_u * 4096;
     uint8_t* lb = la + kTileV * kChunk;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const uint32_t off = (uint32_t)min(wave_u * 64 + 16 * k + lrow, a_rows - 1) * rb + lcol;
-      buffer_to_lds<16>(rsrc_a, off, koff, la + k * 16 * kChunk);
-    }
+    for (int k = 0; k < 4; ++k) buffer_to_lds<16>(rsrc_a, lane_off, soff + k * 1024, la + k * 1024);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) buffer_to_lds<16>(rsrc_b, off_b[k], koff, lb + k * 16 * kChunk);
+    for (int k = 0; k < 4; ++k) buffer_to_lds<16>(rsrc_b, lane_off, soff + k * 1024, lb + k * 1024);
     if constexpr (MODE == kFP8Row) {
       // with a tile's first chunk: its 256 weight-row scales (lane l of wave
       // w moves row 64w + l); they land long before the tile's epilogue
@@ -526,6 +519,28 @@ void score_kernel(ScoreParams p) {
   }
 }
 
+// Packed operand image read by score_kernel: for each 256-row tile and each
+// 64-byte chunk of the rows, one 16 KiB block holding the tile's 256 row
+// pieces in row order, the four 16-byte columns of row r permuted to
+// positions c ^ ((r/4) % 4).  Rows past `rows` repeat the last row.  One
+// thread per 16 bytes: reads run along the source rows, writes land in
+// 64-byte runs.  `units` = n_tiles * 256 * (row_bytes / 16) < 2^32.
+__global__ __launch_bounds__(256) void pack_kernel(const uint8_t* __restrict__ src, uint32_t rows,
+                                                   uint32_t row_bytes, uint32_t units, uint8_t* __restrict__ dst) {
+  const uint32_t pieces = row_bytes / 16;
+  const uint32_t n_chunks = row_bytes / kChunk;
+  for (uint32_t u = blockIdx.x * blockDim.x + threadIdx.x; u < units; u += gridDim.x * blockDim.x) {
+    const uint32_t row = u / pieces;
+    const uint32_t piece = u - row * pieces;
+    const uint32_t kc = piece >> 2, c = piece & 3;
+    const uint32_t tile = row / kTileV, rr = row % kTileV;
+    const uint32_t pos = c ^ ((rr >> 2) & 3);
+    const uint32_t sr = row < rows ? row : rows - 1;
+    const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)sr * row_bytes + piece * 16);
+    *reinterpret_cast<uint4*>(dst + ((size_t)(tile * n_chunks + kc) * kTileV + rr) * kChunk + pos * 16) = v;
+  }
+}
+
 struct MergeParams {
   int n_rows;
   int n_strips;
@@ -591,7 +606,6 @@ void set_score_trace(void* const* events, int n) {
 }
 
 ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V) {
-  (void)d;
   ScorePlan pl{};
   pl.n_ttiles = (int)((n_rows + kTileT - 1) / kTileT);
   pl.n_vtiles = (int)((V + kTileV - 1) / kTileV);
@@ -635,6 +649,13 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V) {
     pl.ws_logit_offset[q] = off;
     off += logit_bytes;
   }
+  // packed operands: W, H (2d bytes per row), Wq, Hq (d bytes per row)
+  const size_t vrows = (size_t)pl.n_vtiles * kTileV, trows = (size_t)pl.n_ttiles * kTileT;
+  const size_t pack_bytes[4] = {vrows * 2 * (size_t)d, trows * 2 * (size_t)d, vrows * (size_t)d, trows * (size_t)d};
+  for (int q = 0; q < 4; ++q) {
+    pl.ws_pack_offset[q] = off;
+    off += align_up(pack_bytes[q], 256);
+  }
   pl.ws_bytes = off;
   return pl;
 }
@@ -656,11 +677,22 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   pp.ids = dsc.token_ids;
   pp.mx_row_bytes = (int)(dsc.d / 32);
 
+  // operands -> packed images in the workspace
+  const void* srcs[4] = {dsc.w, dsc.h, dsc.wq, dsc.hq};
+  const int64_t src_rows[4] = {dsc.V, dsc.n_rows, dsc.V, dsc.n_rows};
+  const int64_t src_tiles[4] = {pl.n_vtiles, pl.n_ttiles, pl.n_vtiles, pl.n_ttiles};
+  for (int q = 0; q < 4; ++q) {
+    const int64_t row_bytes = q < 2 ? 2 * dsc.d : dsc.d;
+    const int64_t units = src_tiles[q] * kTileV * (row_bytes / 16);
+    const unsigned blocks = (unsigned)std::min<int64_t>((units + 255) / 256, 8192);
+    hipLaunchKernelGGL(pack_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint8_t*>(srcs[q]),
+                       (uint32_t)src_rows[q], (uint32_t)row_bytes, (uint32_t)units, ws + pl.ws_pack_offset[q]);
+  }
+
   // pi: bf16 operands
-  pp.a = static_cast<const uint8_t*>(dsc.w);
-  pp.b = static_cast<const uint8_t*>(dsc.h);
-  pp.row_bytes = dsc.d * 2;
-  pp.n_chunks = (int)(pp.row_bytes / kChunk);
+  pp.a = ws + pl.ws_pack_offset[0];
+  pp.b = ws + pl.ws_pack_offset[1];
+  pp.n_chunks = (int)(2 * dsc.d / kChunk);
   pp.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[0]);
   pp.logit = reinterpret_cast<float*>(ws + pl.ws_logit_offset[0]);
   trace(0, s);
@@ -669,10 +701,9 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
 
   // mu: e4m3 operands
   ScoreParams pm = pp;
-  pm.a = static_cast<const uint8_t*>(dsc.wq);
-  pm.b = static_cast<const uint8_t*>(dsc.hq);
-  pm.row_bytes = dsc.d;
-  pm.n_chunks = (int)(pm.row_bytes / kChunk);
+  pm.a = ws + pl.ws_pack_offset[2];
+  pm.b = ws + pl.ws_pack_offset[3];
+  pm.n_chunks = (int)(dsc.d / kChunk);
   pm.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[1]);
   pm.logit = reinterpret_cast<float*>(ws + pl.ws_logit_offset[1]);
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
