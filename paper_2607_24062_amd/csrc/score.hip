@@ -120,6 +120,31 @@ __device__ __forceinline__ float acc_read(float a) {
 }
 
 
+// Workgroup barrier once at most N vector-memory loads of this wave are
+// outstanding and all its LDS reads have completed.  Written as one asm
+// statement (a compiler memory barrier, not a fence): a release fence would
+// also wait for every buffer -> LDS load still in flight, draining the
+// pipeline; ordering against those loads comes from the vmcnt count.
+template <int N>
+__device__ __forceinline__ void wait_loads_and_barrier() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+// Scheduling group of n LDS reads (the builtin takes literal sizes only;
+// n is a constant once the caller's loop is unrolled).
+__device__ __forceinline__ void sched_ds_reads(int n) {
+  switch (n) {
+    case 1: __builtin_amdgcn_sched_group_barrier(0x100, 1, 0); break;
+    case 2: __builtin_amdgcn_sched_group_barrier(0x100, 2, 0); break;
+    case 3: __builtin_amdgcn_sched_group_barrier(0x100, 3, 0); break;
+    case 5: __builtin_amdgcn_sched_group_barrier(0x100, 5, 0); break;
+    case 10: __builtin_amdgcn_sched_group_barrier(0x100, 10, 0); break;
+    case 15: __builtin_amdgcn_sched_group_barrier(0x100, 15, 0); break;
+    default: break;
+  }
+}
+
 // Wait until at most N vector-memory loads of this wave are outstanding
 // (gfx9 s_waitcnt encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt
 // left at their maxima).
@@ -220,9 +245,7 @@ void score_kernel(ScoreParams p) {
     return reinterpret_cast<float*>(lds + NS * (kStageBytes + SB) + (q % Pipe<MODE>::kRowScaleSlots) * kTileV * 4);
   };
 
-  auto issue_chunk = [&](int c, int stg) {
-    const int q = c / p.n_chunks;
-    const int kc = c - q * p.n_chunks;
+  auto issue_chunk = [&](int q, int kc, int stg) {  // chunk kc of the strip's tile q into stage stg
     const int v0 = (vt_begin + q) * kTileV;
     const int a_rows = min(kTileV, p.V - v0);  // valid rows of the vocabulary tile
     const __amdgpu_buffer_rsrc_t rsrc_a = make_rsrc(p.a + (int64_t)(vt_begin + q) * tile_bytes, tile_bytes);
@@ -352,137 +375,220 @@ void score_kernel(ScoreParams p) {
       for (int k = 0; k < 16; ++k) n += min(max(lim - 8 * k, 0), 4);
       nv = (float)n;
     }
-    // keep the 64 tail weights derived from nv inside the epilogue (else they
+    // keep the tail weights derived from nv inside the epilogue (else they
     // are computed before the K loop and held across it)
     asm volatile("v_mov_b32 %0, %0" : "+v"(nv));
+    // The pass, written for instruction-level parallelism (one wave per
+    // SIMD: nothing else hides latencies): all 16 exponents of a block are
+    // formed before any is used, maxima and sums are trees.  The tail tile
+    // (rows past V present) takes its own copy of the code.
+    auto run = [&](auto tail_tag) {
+      constexpr bool kTail = decltype(tail_tag)::value;
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      float rs[16];
-      if constexpr (MODE == kFP8Row) {
-        const float* rsl = rowscales_at(q) + wv * 128 + b * 32 + 4 * g;
+      for (int b = 0; b < 4; ++b) {
+        float rs[16];
+        if constexpr (MODE == kFP8Row) {
+          const float* rsl = rowscales_at(q) + wv * 128 + b * 32 + 4 * g;
 #pragma unroll
-        for (int qq = 0; qq < 4; ++qq) {
-          const f32x4 f = *reinterpret_cast<const f32x4*>(rsl + 8 * qq);
-          rs[4 * qq + 0] = f[0]; rs[4 * qq + 1] = f[1]; rs[4 * qq + 2] = f[2]; rs[4 * qq + 3] = f[3];
+          for (int qq = 0; qq < 4; ++qq) {
+            const f32x4 f = *reinterpret_cast<const f32x4*>(rsl + 8 * qq);
+            rs[4 * qq + 0] = f[0]; rs[4 * qq + 1] = f[1]; rs[4 * qq + 2] = f[2]; rs[4 * qq + 3] = f[3];
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float v[16];
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            v[i] = acc_read(acc[b][j][i]);
+            if constexpr (MODE == kFP8Row) v[i] *= rs[i];
+          }
+          float mx[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) mx[i] = fmaxf(v[2 * i], v[2 * i + 1]);
+#pragma unroll
+          for (int w = 4; w >= 1; w >>= 1)
+#pragma unroll
+            for (int i = 0; i < w; ++i) mx[i] = fmaxf(mx[i], mx[i + w]);
+          const float Mn = fmaxf(M[j], mx[0] * c2[j]);
+          const float dM = M[j] - Mn;
+          const float al = fast_exp2(dM);
+          U[j] = al * fmaf(dM, S[j], U[j]);
+          S[j] *= al;
+          M[j] = Mn;
+          const float nM = -Mn;
+          float t[16], e[16];
+#pragma unroll
+          for (int i = 0; i < 16; ++i) t[i] = fmaf(v[i], c2[j], nM);
+#pragma unroll
+          for (int i = 0; i < 16; ++i) e[i] = fast_exp2(t[i]);
+          if constexpr (kTail) {
+#pragma unroll
+            for (int i = 0; i < 16; ++i) e[i] *= fminf(fmaxf(nv - (float)(16 * b + i), 0.0f), 1.0f);
+          }
+          float s8[8], u8[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            s8[i] = e[2 * i] + e[2 * i + 1];
+            u8[i] = fmaf(e[2 * i + 1], t[2 * i + 1], e[2 * i] * t[2 * i]);
+          }
+#pragma unroll
+          for (int w = 4; w >= 1; w >>= 1)
+#pragma unroll
+            for (int i = 0; i < w; ++i) {
+              s8[i] += s8[i + w];
+              u8[i] += u8[i + w];
+            }
+          S[j] += s8[0];
+          U[j] += u8[0];
+          // finish the update here, ahead of the branch below: otherwise the
+          // pass is sunk past it and the values of all 16 blocks stay live
+          asm volatile("" : "+v"(M[j]), "+v"(S[j]), "+v"(U[j]));
+          // the sampled token a_t: rare branch, taken by the one lane holding it
+          const int rel = id[j] - v0;
+          if ((unsigned)rel < 128u && (rel >> 5) == b && ((rel >> 2) & 1) == g) {
+            float fi = (float)(((rel & 31) >> 3) * 4 + (rel & 3));
+            asm volatile("v_mov_b32 %0, %0" : "+v"(fi));  // keep the weights inside the branch
+            float z = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) z = fmaf(fmaxf(1.0f - fabsf(fi - (float)i), 0.0f), v[i], z);
+            if (tok[j] < p.n_rows && id[j] < p.V) p.logit[tok[j]] = z * cz[j];
+          }
+          __builtin_amdgcn_sched_barrier(0);
         }
       }
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        float v[16];
-        float m = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          v[i] = acc_read(acc[b][j][i]);
-          if constexpr (MODE == kFP8Row) v[i] *= rs[i];
-          m = fmaxf(m, v[i]);
-        }
-        const float Mn = fmaxf(M[j], m * c2[j]);
-        const float dM = M[j] - Mn;
-        const float al = fast_exp2(dM);
-        U[j] = al * fmaf(dM, S[j], U[j]);
-        S[j] *= al;
-        M[j] = Mn;
-        const float nM = -Mn;
-        float s0 = 0.f, u0 = 0.f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const float t = fmaf(v[i], c2[j], nM);
-          float e = fast_exp2(t);
-          if (partial) e *= fminf(fmaxf(nv - (float)(16 * b + i), 0.0f), 1.0f);
-          s0 += e;
-          u0 = fmaf(e, t, u0);
-        }
-        S[j] += s0;
-        U[j] += u0;
-        // finish the update here, ahead of the branch below: otherwise the
-        // pass is sunk past it and the values of all 16 blocks stay live
-        asm volatile("" : "+v"(M[j]), "+v"(S[j]), "+v"(U[j]));
-        // the sampled token a_t: rare branch, taken by the one lane holding it
-        const int rel = id[j] - v0;
-        if ((unsigned)rel < 128u && (rel >> 5) == b && ((rel >> 2) & 1) == g) {
-          float fi = (float)(((rel & 31) >> 3) * 4 + (rel & 3));
-          asm volatile("v_mov_b32 %0, %0" : "+v"(fi));  // keep the weights inside the branch
-          float z = 0.0f;
-#pragma unroll
-          for (int i = 0; i < 16; ++i) z = fmaf(fmaxf(1.0f - fabsf(fi - (float)i), 0.0f), v[i], z);
-          if (tok[j] < p.n_rows && id[j] < p.V) p.logit[tok[j]] = z * cz[j];
-        }
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
+    };
+    if (partial) run(std::true_type{});
+    else run(std::false_type{});
   };
 
   // ---- the pipeline.  Chunks 0..NS-1 are requested up front, one per
-  // stage.  At the end of chunk c (between its last two MFMA groups) every
-  // wave waits for its part of chunk c+1, the workgroup meets at the one
-  // barrier of the chunk, chunk c+NS is requested into c's stage (no wave
-  // reads it any more), and the first fragments of chunk c+1 are read while
-  // the last MFMA group of chunk c runs.
+  // stage.  Fragments are read L MFMA groups ahead of their use, so every LDS
+  // read is covered by 4L MFMAs.  In chunk c the first read of chunk c+1
+  // comes L groups before the end; just before it every wave waits for its
+  // part of chunk c+1, the workgroup meets at the one barrier of the chunk
+  // (after which no wave reads chunk c's stage any more) and chunk c+NS is
+  // requested into that stage.  The steady-state chunk body is straight-line
+  // code; the last NS chunks of a workgroup take a second copy that waits
+  // for all loads and requests nothing.
+  constexpr int L = (MODE == kBF16) ? 2 : 1;
+  int qi = 0, kci = 0;  // tile and chunk of the next chunk to request
+  auto advance_issue = [&]() {
+    if (++kci == p.n_chunks) {
+      kci = 0;
+      ++qi;
+    }
+  };
 #pragma unroll
-  for (int c = 0; c < NS; ++c)
-    if (c < n_iter) issue_chunk(c, c);
+  for (int c = 0; c < NS; ++c) {
+    if (c < n_iter) {
+      issue_chunk(qi, kci, c);
+      advance_issue();
+    }
+  }
   if (n_iter < NS) wait_vmcnt<0>();
   else wait_vmcnt<(NS - 1) * LPC>();
   __syncthreads();
-  FragT a_cur, a_nxt, b_cur[4], b_nxt[4];
-  int sa_cur = 0, sa_nxt = 0, sb_cur[4] = {0, 0, 0, 0}, sb_nxt[4] = {0, 0, 0, 0};
-  a_cur = read_a(0, 0);
-  read_b(0, 0, b_cur);
-  if constexpr (MODE == kMX) {
-    sa_cur = read_sa(0, 0);
-    read_sb(0, sb_cur);
-  }
-  a_nxt = a_cur;
+
+  // Fragments a chunk starts with (its first L groups' A, its first B step,
+  // MX scales).  Two sets alternate between even and odd chunks (every tile
+  // has an even number of chunks), so the next chunk's fragments are read
+  // straight into the registers it will use.
+  struct Frags {
+    FragT a[L], b[4];
+    int sa[L], sb[4];
+  };
+  Frags f0, f1;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) b_nxt[j] = b_cur[j];
+  for (int l = 0; l < L; ++l) {
+    f0.a[l] = read_a(0, l);
+    f0.sa[l] = 0;
+    if constexpr (MODE == kMX) f0.sa[l] = read_sa(0, l);
+  }
+  read_b(0, 0, f0.b);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) f0.sb[j] = 0;
+  if constexpr (MODE == kMX) read_sb(0, f0.sb);
+
+  // LDS read instructions issued in group k (for group k + L)
+  auto reads_at = [](int k) constexpr {
+    const int t = k + L, tt = t % G;
+    constexpr int per_frag = (MODE == kBF16) ? 1 : 2;
+    int n = per_frag + (MODE == kMX ? 1 : 0);                               // A (+ its MX scale)
+    if (tt % 4 == 0) n += 4 * per_frag + (MODE == kMX && tt == 0 ? 4 : 0);  // B of a new step
+    return n;
+  };
+  int stg = 0;  // stage of the current chunk
+  auto chunk = [&](auto steady_tag, int it, Frags& cur, Frags& nxt) {
+    constexpr bool kSteady = decltype(steady_tag)::value;
+    const bool has_next = kSteady || it + 1 < n_iter;
+    const int nst = stg + 1 == NS ? 0 : stg + 1;
+    FragT af[G];       // A of this chunk's groups
+    FragT bf[2][4];    // B of this chunk's K steps (BF16: 2, FP8: 1)
+    int sa[G];
+#pragma unroll
+    for (int l = 0; l < L; ++l) {
+      af[l] = cur.a[l];
+      sa[l] = cur.sa[l];
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) bf[0][j] = cur.b[j];
+#pragma unroll
+    for (int k = 0; k < G; ++k) {
+      const int t = k + L;  // group whose fragments are read now
+      if (t == G && has_next) {
+        // chunk it+1 must have landed (chunks it+2 .. it+NS-1 may be in flight)
+        if constexpr (kSteady) wait_loads_and_barrier<(NS - 2) * LPC>();
+        else wait_loads_and_barrier<0>();
+        if (kSteady || it + NS < n_iter) {
+          issue_chunk(qi, kci, stg);
+          advance_issue();
+        }
+      }
+      if (t < G) {
+        af[t] = read_a(stg, t);
+        sa[t] = 0;
+        if constexpr (MODE == kMX) sa[t] = read_sa(stg, t);
+        if (t % 4 == 0) read_b(stg, t, bf[t / 4]);  // BF16: second K step
+      } else if (has_next) {
+        nxt.a[t - G] = read_a(nst, t - G);
+        nxt.sa[t - G] = 0;
+        if constexpr (MODE == kMX) nxt.sa[t - G] = read_sa(nst, t - G);
+        if (t == G) {
+          read_b(nst, 0, nxt.b);
+          if constexpr (MODE == kMX) read_sb(nst, nxt.sb);
+        }
+      }
+      mfma_group(k, af[k], bf[k / 4], sa[k], cur.sb);
+      if constexpr (kSteady) {
+        // keep this group's LDS reads ahead of its MFMAs (the scheduler
+        // would otherwise sink each read to just before its use)
+        sched_ds_reads(reads_at(k));
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // 4 MFMAs
+      }
+    }
+    stg = nst;
+  };
 
   int it = 0;
   for (int q = 0; q < vt_end - vt_begin; ++q) {
-    for (int kc = 0; kc < p.n_chunks; ++kc, ++it) {
-      const int stg = it % NS;
-#pragma unroll
-      for (int grp = 0; grp < G; ++grp) {
-        const bool new_step = grp + 1 < G && ((grp + 1) & 3) == 0;  // BF16: second K step
-        if (grp + 1 < G) {
-          a_nxt = read_a(stg, grp + 1);
-          if constexpr (MODE == kMX) sa_nxt = read_sa(stg, grp + 1);
-          if (new_step) read_b(stg, grp + 1, b_nxt);
-        } else if (it + 1 < n_iter) {
-          // chunk it+1 must have landed; chunks it+2 .. it+NS-1 may be in flight
-          const int ahead = min(NS - 2, n_iter - 2 - it);
-          if (ahead >= NS - 2) wait_vmcnt<(NS - 2) * LPC>();
-          else if (ahead == 2) wait_vmcnt<2 * LPC>();
-          else if (ahead == 1) wait_vmcnt<LPC>();
-          else wait_vmcnt<0>();
-          __syncthreads();
-          if (it + NS < n_iter) issue_chunk(it + NS, stg);
-          const int nst = (it + 1) % NS;
-          a_nxt = read_a(nst, 0);
-          read_b(nst, 0, b_nxt);
-          if constexpr (MODE == kMX) {
-            sa_nxt = read_sa(nst, 0);
-            read_sb(nst, sb_nxt);
-          }
-        }
-        mfma_group(grp, a_cur, b_cur, sa_cur, sb_cur);
-        a_cur = a_nxt;
-        sa_cur = sa_nxt;
-        if (new_step || grp + 1 == G) {
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            b_cur[j] = b_nxt[j];
-            sb_cur[j] = sb_nxt[j];
-          }
-        }
-      }
-      if (kc == p.n_chunks - 1) {
-        epilogue(vt_begin + q, q);
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
-      }
+    // steady chunks: [0, kc_steady); the rest request nothing new or only
+    // while requests remain, and wait for every load
+    const int kc_steady = min(p.n_chunks, max(0, n_iter - NS - it));
+    int kc = 0;
+    for (; kc + 1 < kc_steady; kc += 2, it += 2) {
+      chunk(std::true_type{}, it, f0, f1);
+      chunk(std::true_type{}, it + 1, f1, f0);
     }
+    for (; kc < p.n_chunks; kc += 2, it += 2) {
+      chunk(std::false_type{}, it, f0, f1);
+      chunk(std::false_type{}, it + 1, f1, f0);
+    }
+    epilogue(vt_begin + q, q);
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
   }
   __syncthreads();  // every wave is done with the stages before LDS is reused
 
