@@ -8,6 +8,11 @@ happens once per weight version and is reported separately.
 
 Usage: python bench.py [--gpus 1] [--steps 5] [--warmup 2] [--workload q8b]
 Prints progress on stderr and ONE JSON line on stdout.
+
+python bench.py --counters runs a plain copy of known size and one step, for
+the FETCH_SIZE / WRITE_SIZE passes that give roofline.traffic (see
+paper_2607_24062_amd/profiling.py); the traffic is read back from
+profiles/score_<workload>_traffic.md while it matches the kernel sources.
 """
 from __future__ import annotations
 
@@ -38,6 +43,8 @@ def main():
     ap.add_argument("--workload", default="q8b", choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--counters", action="store_true",
+                    help="copy calibration + one step only (for rocprofv3 --pmc passes)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this path runs on a single MI355X "
@@ -45,7 +52,7 @@ def main():
         sys.exit(2)
 
     import torch
-    from paper_2607_24062_amd import acrl
+    from paper_2607_24062_amd import acrl, profiling
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -123,6 +130,18 @@ def main():
             rev[2].record()
         return red
 
+    if args.counters:
+        # a plain copy of COPY_BYTES (read and written once), then one step
+        src = torch.ones(profiling.COPY_BYTES // 2, dtype=torch.bfloat16, device=dev)
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+        step()
+        torch.cuda.synchronize()
+        log("counters run done")
+        return
+
     # ---------------- warmup (step 0 calibrates X, Sec. 4.1)
     t0 = time.time()
     red = step()
@@ -157,11 +176,14 @@ def main():
     t_mu = np.mean([tev[k][1].elapsed_time(tev[k][2]) for k in range(K)])
     t_merge = np.mean([tev[k][2].elapsed_time(tev[k][3]) for k in range(K)])
     t_qh = np.mean([qev[k][0].elapsed_time(qev[k][1]) for k in range(K)])
+    # the score call = operand packing + pi + mu + merge (events: end of quantize -> start of reduce)
+    t_call = np.mean([qev[k][1].elapsed_time(rev[k][0]) for k in range(K)])
+    t_pack = max(t_call - t_pi - t_mu - t_merge, 0.0)
     t_red = np.mean([rev[k][0].elapsed_time(rev[k][1]) for k in range(K)])
     t_ctl = np.mean([rev[k][1].elapsed_time(rev[k][2]) for k in range(K)])
     stats = red["stats"].cpu().numpy()
-    log("per step %.3f ms | quantize H %.3f | pi %.3f | mu %.3f | merge %.3f | reduce %.3f | "
-        "controller %.3f ms" % (ms_per_step, t_qh, t_pi, t_mu, t_merge, t_red, t_ctl))
+    log("per step %.3f ms | quantize H %.3f | pack %.3f | pi %.3f | mu %.3f | merge %.3f | reduce %.3f | "
+        "controller %.3f ms" % (ms_per_step, t_qh, t_pack, t_pi, t_mu, t_merge, t_red, t_ctl))
     log("batch stats:", dict(zip(acrl.STAT_NAMES, [float(x) for x in stats])))
 
     flops = 2.0 * T * V * d           # per precision, algorithmic
@@ -176,6 +198,14 @@ def main():
                "frac": round(ach_mu / PEAK_TFLOPS["fp8"], 4), "traffic": None,
                "avg_ms": round(float(t_mu), 4), "flops_per_launch": flops}
     dominant = roof_pi if t_pi >= t_mu else roof_mu
+    # HBM traffic of each score kernel from the committed counter summary, if current
+    tr = profiling.load_traffic(os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                                             "score_%s_traffic.md" % w.name))
+    mu_kernel = "score_kernel<%d>" % {inputs.PER_TENSOR: 1, inputs.PER_ROW: 2, inputs.MX32: 3}[w.scaling]
+    for roof, kname in ((roof_pi, "score_kernel<0>"), (roof_mu, mu_kernel)):
+        if tr is not None and kname in tr["kernels"]:
+            roof["traffic"] = round(tr["kernels"][kname]["traffic_bytes"])
+            roof["traffic_unit"] = "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     # fraction of the combined MFMA roofline: ideal time at both peaks / measured step time
     ideal_ms = (flops / (PEAK_TFLOPS["bf16"] * 1e12) + flops / (PEAK_TFLOPS["fp8"] * 1e12)) * 1e3
     q_bytes = T * d * 3 + (T * d * 2 if w.scaling == inputs.PER_TENSOR else 0)
@@ -197,7 +227,8 @@ def main():
         "config": {"workload": w.describe(), "valid_tokens": T, "slots": w.slots,
                    "ids": "uniform over the vocabulary (work is id-independent)",
                    "mfma_frac_combined": round(ideal_ms / ms_per_step, 4),
-                   "kernel_ms": {"quantize_h": round(float(t_qh), 4), "score_pi": round(float(t_pi), 4),
+                   "kernel_ms": {"quantize_h": round(float(t_qh), 4), "pack": round(float(t_pack), 4),
+                                 "score_pi": round(float(t_pi), 4),
                                  "score_mu": round(float(t_mu), 4), "merge": round(float(t_merge), 4),
                                  "reduce": round(float(t_red), 4), "controller": round(float(t_ctl), 4)},
                    "quantize_h_GBps": round(q_bytes / (t_qh * 1e-3) / 1e9, 1),

@@ -1,0 +1,144 @@
+"""rocprofv3 summaries for the score kernels (observability, not the compute path).
+
+Turns rocprofv3 CSV output (``--output-format csv``) into the short markdown
+summaries kept under ``profiles/`` and derives the HBM traffic of a kernel
+from two counter passes:
+
+    rocprofv3 --pmc FETCH_SIZE --output-format csv -d DIR -o fetch -- python bench.py --counters
+    rocprofv3 --pmc WRITE_SIZE --output-format csv -d DIR -o write -- python bench.py --counters
+
+``bench.py --counters`` first runs a plain elementwise copy of a known size
+(reads and writes ``COPY_BYTES``), so the counters, which report KiB per
+dispatch, are scaled by what they read for that copy.
+
+Command line:
+    python -m paper_2607_24062_amd.profiling stats CSV TITLE COMMAND > profiles/x.md
+    python -m paper_2607_24062_amd.profiling traffic FETCH_CSV WRITE_CSV TITLE COMMAND > profiles/y.md
+"""
+from __future__ import annotations
+
+import csv
+import hashlib
+import json
+import os
+import re
+import sys
+
+COPY_BYTES = 1 << 30          # the calibration copy: 1 GiB read, 1 GiB written
+COPY_KERNEL = "neg"           # it is torch.neg(out=...) on a bf16 tensor
+KERNEL_SOURCES = ("csrc/score.hip", "csrc/acrl_internal.h")
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def source_digest() -> str:
+    """sha256 over the score kernel's sources: counters are stale once it changes."""
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(_HERE, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def short_name(name: str) -> str:
+    n = name.replace("acrl::(anonymous namespace)::", "").replace("void ", "")
+    return n.split("(")[0]
+
+
+def kernel_stats(path: str):
+    rows = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            rows.append({"name": short_name(r["Name"]), "calls": int(r["Calls"]),
+                         "avg_ms": float(r["AverageNs"]) / 1e6, "min_ms": float(r["MinNs"]) / 1e6,
+                         "max_ms": float(r["MaxNs"]) / 1e6, "pct": float(r["Percentage"])})
+    return rows
+
+
+def stats_markdown(path: str, title: str, command: str) -> str:
+    out = ["# %s" % title, "", "Command (from the repository root on one MI355X):", "", "```",
+           command, "```", "", "| kernel | calls | average ms | min ms | max ms | share |",
+           "|---|---|---|---|---|---|"]
+    for r in kernel_stats(path):
+        out.append("| %s | %d | %.4f | %.4f | %.4f | %.2f%% |" % (
+            r["name"], r["calls"], r["avg_ms"], r["min_ms"], r["max_ms"], r["pct"]))
+    return "\n".join(out) + "\n"
+
+
+def counter_means(path: str, counter: str):
+    """Mean value of `counter` per dispatch, by kernel short name."""
+    acc = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            acc.setdefault(short_name(r["Kernel_Name"]), []).append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def traffic(fetch_csv: str, write_csv: str):
+    """Per-dispatch HBM bytes of each acrl kernel, scaled by the copy calibration."""
+    fetch = counter_means(fetch_csv, "FETCH_SIZE")
+    write = counter_means(write_csv, "WRITE_SIZE")
+    copy_f = [v for k, v in fetch.items() if COPY_KERNEL in k.lower()]
+    copy_w = [v for k, v in write.items() if COPY_KERNEL in k.lower()]
+    if not copy_f or not copy_w:
+        raise RuntimeError("calibration copy kernel not found in the counter files")
+    f_scale = COPY_BYTES / (copy_f[0] * 1024.0)
+    w_scale = COPY_BYTES / (copy_w[0] * 1024.0)
+    res = {"copy_fetch_kib": copy_f[0], "copy_write_kib": copy_w[0],
+           "fetch_scale": f_scale, "write_scale": w_scale, "kernels": {}}
+    for k in sorted(set(fetch) | set(write)):
+        if COPY_KERNEL in k.lower():
+            continue
+        fb = fetch.get(k, 0.0) * 1024.0 * f_scale
+        wb = write.get(k, 0.0) * 1024.0 * w_scale
+        res["kernels"][k] = {"fetch_bytes": fb, "write_bytes": wb, "traffic_bytes": fb + wb}
+    return res
+
+
+def traffic_markdown(fetch_csv: str, write_csv: str, title: str, command: str) -> str:
+    t = traffic(fetch_csv, write_csv)
+    t["source_sha256"] = source_digest()
+    out = ["# %s" % title, "", "Commands (from the repository root on one MI355X), one counter per pass:",
+           "", "```", command, "```", "",
+           "FETCH_SIZE / WRITE_SIZE are KiB per dispatch; each is scaled by its reading for a plain",
+           "elementwise copy of %d bytes (fetch x%.4f, write x%.4f)." % (COPY_BYTES, t["fetch_scale"],
+                                                                        t["write_scale"]),
+           "", "| kernel | fetch GB | write GB | traffic GB |", "|---|---|---|---|"]
+    for k, v in t["kernels"].items():
+        out.append("| %s | %.3f | %.3f | %.3f |" % (k, v["fetch_bytes"] / 1e9, v["write_bytes"] / 1e9,
+                                                 v["traffic_bytes"] / 1e9))
+    out += ["", "Machine-readable (bench.py reads it while source_sha256 matches the kernel sources):",
+            "", "```json", json.dumps(t, indent=1, sort_keys=True), "```"]
+    return "\n".join(out) + "\n"
+
+
+def load_traffic(md_path: str):
+    """The JSON block of a traffic summary, or None if absent or stale."""
+    if not os.path.exists(md_path):
+        return None
+    with open(md_path) as f:
+        text = f.read()
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return None
+    t = json.loads(m.group(1))
+    if t.get("source_sha256") != source_digest():
+        return None
+    return t
+
+
+def main(argv):
+    if len(argv) >= 4 and argv[0] == "stats":
+        sys.stdout.write(stats_markdown(argv[1], argv[2], argv[3]))
+    elif len(argv) >= 5 and argv[0] == "traffic":
+        sys.stdout.write(traffic_markdown(argv[1], argv[2], argv[3], argv[4]))
+    else:
+        sys.stderr.write(__doc__)
+        return 2
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main(sys.argv[1:]))
