@@ -25,6 +25,7 @@ LIB = os.path.join(HERE, "libacrl_oracle.so")
 PER_TENSOR, PER_ROW, MX32 = 0, 1, 2
 ROUND_NEAREST_EVEN, ROUND_TOWARD_ZERO = 0, 1
 Y_GROUP, Y_SEQUENCE, Y_BATCH = 0, 1, 2
+CTRL_ACRL, CTRL_TIS, CTRL_MIS, CTRL_CONTINUOUS, CTRL_FALLBACK = 0, 1, 2, 3, 4
 
 # indices of the batch statistics vector (mirrors the enum in acrl_oracle.h)
 STAT_Y_BATCH = 0
@@ -86,7 +87,7 @@ def lib() -> ctypes.CDLL:
         L.acrl_ref_discrepancy_reduce.argtypes = [I64, I64, P, P, P, P, P, P, I64] + [P] * 8
         L.acrl_ref_controller_step.restype = I32
         L.acrl_ref_controller_step.argtypes = [I64, I64, P, P, P, P, P, I32, I32, P, P, P,
-                                               D, D, D, P, P]
+                                               D, D, D, I32, D, P, P]
         L.acrl_ref_reference_x.restype = I32
         L.acrl_ref_reference_x.argtypes = [P, P, I64, P]
         L.acrl_ref_sample_inverse_cdf.restype = I32
@@ -231,7 +232,7 @@ def discrepancy_reduce(B: int, L: int, logp_pi, logp_mu, mask, group_of_seq, n_g
 # ---------------------------------------------------------------- a8
 def controller_step(B: int, L: int, mask, group_of_seq, logp_pi, logp_mu, adv,
                     adv_per_token: bool, y_level: int, seq_mean_d, group_y, stats,
-                    X: float, gamma: float, C: float):
+                    X: float, gamma: float, C: float, mode: int = 0, k: float = 1.0):
     m = _c(mask, np.uint8).reshape(-1)
     g = _c(group_of_seq, np.int32)
     lp_p, lp_m = _c(logp_pi, np.float64).reshape(-1), _c(logp_mu, np.float64).reshape(-1)
@@ -243,7 +244,8 @@ def controller_step(B: int, L: int, mask, group_of_seq, logp_pi, logp_mu, adv,
     weight = np.zeros(B * L)
     _check(lib().acrl_ref_controller_step(B, L, _p(m), _p(g), _p(lp_p), _p(lp_m), _p(a),
                                           int(bool(adv_per_token)), y_level, _p(smd), _p(gy),
-                                          _p(st), X, gamma, C, _p(alpha), _p(weight)),
+                                          _p(st), X, gamma, C, int(mode), float(k), _p(alpha),
+                                          _p(weight)),
            "controller_step")
     return alpha, weight
 

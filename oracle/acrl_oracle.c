@@ -461,9 +461,11 @@ int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
                              const double* adv, int adv_per_token, int y_level,
                              const double* seq_mean_d, const double* group_y,
                              const double* stats, double X, double gamma, double C,
-                             double* alpha, double* weight) {
+                             int mode, double k, double* alpha, double* weight) {
   if (B < 0 || L < 0 || !mask || !logp_pi || !logp_mu || !adv || !weight) return -1;
   if (!(X > 0.0) || !(gamma > 0.0) || !(C > 1.0)) return -1;
+  if (mode < REF_CTRL_ACRL || mode > REF_CTRL_FALLBACK) return -1;
+  if (mode == REF_CTRL_CONTINUOUS && !(k > 0.0)) return -1;
   for (int64_t i = 0; i < B; ++i) {
     double Y;
     if (y_level == REF_Y_SEQUENCE) {
@@ -478,15 +480,33 @@ int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
     } else {
       return -1;
     }
+    /* Eq. mis_objective: the sequence's probability ratio pi(a_i)/mu(a_i),
+     * the product of its token ratios */
+    double rho_seq = 1.0;
+    if (mode == REF_CTRL_MIS)
+      for (int64_t j = 0; j < L; ++j)
+        if (mask[i * L + j]) rho_seq *= exp(logp_pi[i * L + j] - logp_mu[i * L + j]);
     for (int64_t j = 0; j < L; ++j) {
       const int64_t t = i * L + j;
       double a = 0.0, wt = 0.0;
       if (mask[t]) {
         const double A = adv_per_token ? adv[t] : adv[i];
-        a = gamma * sign_of(A) * (1.0 - Y / X);
         const double ratio = exp(logp_pi[t] - logp_mu[t]); /* pi / mu */
-        const double rho = pow(ratio, a);
-        wt = rho < C ? rho : C;
+        if (mode == REF_CTRL_TIS) {
+          a = 1.0;
+          wt = ratio < C ? ratio : C;
+        } else if (mode == REF_CTRL_MIS) {
+          a = 1.0;
+          wt = rho_seq <= C ? rho_seq : 0.0;
+        } else if (mode == REF_CTRL_FALLBACK && Y < X) {
+          a = 0.0;
+          wt = 1.0;
+        } else {
+          if (mode == REF_CTRL_CONTINUOUS) a = -k * sign_of(A);
+          else a = gamma * sign_of(A) * (1.0 - Y / X);
+          const double rho = pow(ratio, a);
+          wt = rho < C ? rho : C;
+        }
       }
       if (alpha) alpha[t] = a;
       weight[t] = wt;

@@ -30,6 +30,11 @@ enum { REF_PER_TENSOR = 0, REF_PER_ROW = 1, REF_MX32 = 2 };
 enum { REF_ROUND_NEAREST_EVEN = 0, REF_ROUND_TOWARD_ZERO = 1 };
 /* Granularity of Y in alpha = gamma*sign(A)*(1 - Y/X) (Sec. 4.1).            */
 enum { REF_Y_GROUP = 0, REF_Y_SEQUENCE = 1, REF_Y_BATCH = 2 };
+/* Weighting rule of the controller step: the paper's ACRL (Eq. ACRL), the
+ * token-level TIS it builds on (Eq. tis_objective), sequence-level MIS
+ * (Eq. mis_objective), and the two one-sided ablations of Sec. 5
+ * ("continuous reduction", "fallback to GRPO"). */
+enum { REF_CTRL_ACRL = 0, REF_CTRL_TIS = 1, REF_CTRL_MIS = 2, REF_CTRL_CONTINUOUS = 3, REF_CTRL_FALLBACK = 4 };
 
 /* Indices into the batch statistics vector written by the reduce. */
 enum {
@@ -109,14 +114,21 @@ int acrl_ref_discrepancy_reduce(int64_t B, int64_t L,
  * adv: [B] (one advantage per response, GRPO) or [B*L] (adv_per_token=1).
  * Y is read from seq_mean_d[i], group_y[group_of_seq[i]] or stats[0]
  * according to y_level.  Outputs alpha, weight [B*L]; masked slots -> 0.
- * Requires X > 0, gamma > 0, C > 1.                                        */
+ * mode (REF_CTRL_*), per valid token t of sequence i, rho_t = pi/mu:
+ *   ACRL:       alpha = gamma sign(A) (1 - Y/X), weight = min(rho_t^alpha, C)
+ *   TIS:        alpha = 1,                       weight = min(rho_t, C)
+ *   MIS:        alpha = 1, weight = rho_i if rho_i <= C else 0, with
+ *               rho_i = product of rho_t over the valid tokens of i
+ *   CONTINUOUS: alpha = -k sign(A),              weight = min(rho_t^alpha, C)
+ *   FALLBACK:   Y < X: alpha = 0, weight = 1 (plain GRPO); else as ACRL
+ * Requires X > 0, gamma > 0, C > 1, k > 0 (k is read in CONTINUOUS only).  */
 int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
                              const int32_t* group_of_seq,
                              const double* logp_pi, const double* logp_mu,
                              const double* adv, int adv_per_token, int y_level,
                              const double* seq_mean_d, const double* group_y,
                              const double* stats, double X, double gamma, double C,
-                             double* alpha, double* weight);
+                             int mode, double k, double* alpha, double* weight);
 
 /* Reference X (Sec. 4.1): mean of the per-group discrepancy over the
  * non-empty groups (group_nseq > 0) of the step-0 batches.                 */

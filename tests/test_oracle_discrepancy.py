@@ -232,3 +232,92 @@ def test_controller_rejects_bad_hyperparameters():
     for X, gamma, C in ((0.0, 0.5, 3.0), (0.01, 0.0, 3.0), (0.01, 0.5, 1.0), (-1, 0.5, 3)):
         with pytest.raises(ValueError):
             _ctrl_one(0.2, 0.4, 1.0, 0.02, X, gamma, C)
+
+
+# ------------------------------------------------------------ controller modes
+# TIS (Eq. tis_objective), MIS (Eq. mis_objective) and the two one-sided
+# ablations of Sec. 5 (continuous reduction, fallback to GRPO), pinned by
+# their closed forms.
+def _ctrl_mode(pi, mu, A, Y, mode, k=1.0, X=0.013, gamma=0.65, C=3.0):
+    alpha, w = oracle.controller_step(1, 1, np.ones(1, np.uint8), np.zeros(1, np.int32),
+                                      np.log([pi]), np.log([mu]), np.array([A]), False,
+                                      oracle.Y_BATCH, None, None,
+                                      np.array([Y] + [0.0] * (oracle.N_STATS - 1)), X, gamma, C,
+                                      mode=mode, k=k)
+    return alpha[0], w[0]
+
+
+@pytest.mark.parametrize("pi,mu,want", [(0.2, 0.4, 0.5), (0.4, 0.2, 2.0), (0.01, 0.5, 0.02),
+                                        (0.9, 0.1, 3.0), (0.3, 0.3, 1.0)])
+def test_tis_is_truncated_ratio(pi, mu, want):
+    for A, Y in ((1.0, 0.026), (-1.0, 0.0065), (0.0, 0.013)):
+        alpha, w = _ctrl_mode(pi, mu, A, Y, oracle.CTRL_TIS)
+        assert alpha == 1.0
+        assert abs(w - want) < 1e-12
+
+
+def test_tis_equals_acrl_at_gamma_one_y_zero():
+    for pi, mu in ((0.2, 0.4), (0.4, 0.2), (0.9, 0.1)):
+        _, w_acrl = _ctrl_mode(pi, mu, 1.0, 0.0, oracle.CTRL_ACRL, gamma=1.0)
+        _, w_tis = _ctrl_mode(pi, mu, 1.0, 0.0, oracle.CTRL_TIS)
+        assert abs(w_acrl - w_tis) < 1e-12
+
+
+def test_mis_weights_whole_sequences():
+    # 3 sequences of 4 slots; token log-ratios chosen so the sequence ratios
+    # are 2 (kept), 4 (> C = 3: masked to 0) and 1/2 (kept)
+    B, L = 3, 4
+    mask = np.array([[1, 1, 1, 1], [1, 1, 1, 0], [1, 1, 0, 0]], np.uint8)
+    lp_mu = np.log(np.full((B, L), 0.3))
+    lr = np.zeros((B, L))
+    lr[0, :4] = [math.log(2) * f for f in (0.1, 0.2, 0.3, 0.4)]
+    lr[1, :3] = [math.log(4) / 3] * 3
+    lr[1, 3] = 5.0                       # a masked slot must not count
+    lr[2, :2] = [-math.log(2) * 0.75, -math.log(2) * 0.25]
+    lp_pi = lp_mu + lr
+    adv = np.array([1.0, -1.0, 0.0])
+    stats = np.zeros(oracle.N_STATS)
+    alpha, w = oracle.controller_step(B, L, mask, np.zeros(B, np.int32), lp_pi, lp_mu, adv, False,
+                                      oracle.Y_BATCH, None, None, stats, 0.013, 0.65, 3.0,
+                                      mode=oracle.CTRL_MIS)
+    w = w.reshape(B, L)
+    want = [2.0, 0.0, 0.5]
+    for i in range(B):
+        for j in range(L):
+            if mask[i, j]:
+                assert abs(w[i, j] - want[i]) < 1e-12
+            else:
+                assert w[i, j] == 0.0
+
+
+@pytest.mark.parametrize("k", [1.0, 3.0])
+def test_continuous_reduction_fixed_alpha(k):
+    # alpha = -k for A > 0 (quadrants I, II), +k for A < 0 (III, IV), any Y
+    for Y in (0.026, 0.0065):
+        a, w = _ctrl_mode(0.2, 0.4, 1.0, Y, oracle.CTRL_CONTINUOUS, k=k, C=100.0)
+        assert a == -k and abs(w - 2.0 ** k) < 1e-12
+        a, w = _ctrl_mode(0.4, 0.2, 1.0, Y, oracle.CTRL_CONTINUOUS, k=k, C=100.0)
+        assert a == -k and abs(w - 0.5 ** k) < 1e-12
+        a, w = _ctrl_mode(0.4, 0.2, -1.0, Y, oracle.CTRL_CONTINUOUS, k=k, C=100.0)
+        assert a == k and abs(w - 2.0 ** k) < 1e-12
+        a, w = _ctrl_mode(0.4, 0.2, 0.0, Y, oracle.CTRL_CONTINUOUS, k=k)
+        assert a == 0 and w == 1.0
+    # clip: 2^3 = 8 > C = 3
+    assert _ctrl_mode(0.2, 0.4, 1.0, 0.02, oracle.CTRL_CONTINUOUS, k=3.0)[1] == 3.0
+
+
+def test_fallback_is_grpo_below_x_and_acrl_above():
+    for pi, mu, A in ((0.2, 0.4, 1.0), (0.4, 0.2, -1.0), (0.01, 0.5, 1.0)):
+        a, w = _ctrl_mode(pi, mu, A, 0.0065, oracle.CTRL_FALLBACK)
+        assert a == 0.0 and w == 1.0
+        for Y in (0.013, 0.026):
+            got = _ctrl_mode(pi, mu, A, Y, oracle.CTRL_FALLBACK)
+            want = _ctrl_mode(pi, mu, A, Y, oracle.CTRL_ACRL)
+            assert got == want
+
+
+def test_controller_rejects_bad_mode_or_k():
+    with pytest.raises(ValueError):
+        _ctrl_mode(0.2, 0.4, 1.0, 0.02, 7)
+    with pytest.raises(ValueError):
+        _ctrl_mode(0.2, 0.4, 1.0, 0.02, oracle.CTRL_CONTINUOUS, k=0.0)
