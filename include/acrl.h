@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ACRL_ABI_VERSION 1
+#define ACRL_ABI_VERSION 2
 
 typedef int acrl_status;
 enum {
@@ -65,6 +65,15 @@ typedef enum {
   ACRL_Y_SEQUENCE = 1,        /* Y of the response itself                           */
   ACRL_Y_BATCH = 2            /* Y of the whole batch                               */
 } acrl_y_level;
+
+/* Weighting rule of acrl_controller_step. */
+typedef enum {
+  ACRL_CTRL_ACRL = 0,         /* Eq. ACRL: rho = (pi/mu)^alpha, alpha = gamma sign(A)(1 - Y/X) */
+  ACRL_CTRL_TIS = 1,          /* Eq. tis_objective: token-level min(pi/mu, C)                  */
+  ACRL_CTRL_MIS = 2,          /* Eq. mis_objective: the sequence ratio, 0 where it exceeds C   */
+  ACRL_CTRL_CONTINUOUS = 3,   /* Sec. 5 ablation "continuous reduction": alpha = -k sign(A)    */
+  ACRL_CTRL_FALLBACK = 4      /* Sec. 5 ablation "fallback to GRPO": weight 1 when Y < X       */
+} acrl_ctrl_mode;
 
 /* Slots of the batch statistics vector (double[ACRL_N_STATS]). */
 enum {
@@ -222,15 +231,24 @@ acrl_status acrl_discrepancy_reduce(const acrl_reduce_desc* desc, void* stream);
 /* ======================================================================== */
 /* a8  acrl_controller_step -- ACRL per-token weights                       */
 /* ======================================================================== *
- * Eq. ACRL: the clipped surrogate of every valid token is weighted by
- * min(rho, C) with rho = (pi(a_t)/mu(a_t))^alpha and
+ * Eq. ACRL (mode ACRL_CTRL_ACRL): the clipped surrogate of every valid token
+ * is weighted by min(rho, C) with rho = (pi(a_t)/mu(a_t))^alpha and
  * alpha = gamma * sign(A) * (1 - Y/X) (sign(0) = 0).  Computed as
  * weight = exp(min(alpha * (logp_pi - logp_mu), ln C)), which equals
  * min(rho, C).  Masked slots get alpha = 0 and weight = 0.
  * Y comes from seq_mean_d[i], group_y[group_of_seq[i]] or
  * stats[ACRL_STAT_Y_BATCH] per y_level (outputs of acrl_discrepancy_reduce).
- * Requirements: X > 0, gamma > 0, C > 1 (Sec. 4.1); the array y_level reads
- * must be non-NULL.
+ * Other modes (alpha output in parentheses):
+ *   ACRL_CTRL_TIS        weight = min(pi/mu, C)                     (1)
+ *   ACRL_CTRL_MIS        weight = rho_i if rho_i <= C, else 0, for every valid
+ *                        token of sequence i, rho_i = exp(seq_sum_logratio[i])
+ *                        (the output of acrl_discrepancy_reduce)       (1)
+ *   ACRL_CTRL_CONTINUOUS alpha = -k sign(A), weight = min((pi/mu)^alpha, C)
+ *   ACRL_CTRL_FALLBACK   Y < X: weight = 1 (plain GRPO)             (0);
+ *                        otherwise as ACRL_CTRL_ACRL
+ * Requirements: X > 0, gamma > 0, C > 1 (Sec. 4.1); k > 0 for CONTINUOUS;
+ * seq_sum_logratio non-NULL for MIS; the arrays y_level reads non-NULL for
+ * ACRL and FALLBACK.
  */
 typedef struct acrl_controller_desc {
   int64_t B;
@@ -251,6 +269,9 @@ typedef struct acrl_controller_desc {
   float C;                      /* clip, > 1                                                */
   float* alpha;                 /* [B*L] out, nullable                                      */
   float* weight;                /* [B*L] out                                                */
+  int32_t mode;                 /* acrl_ctrl_mode (0 = ACRL)                                 */
+  float k;                      /* |alpha| of ACRL_CTRL_CONTINUOUS, > 0                     */
+  const double* seq_sum_logratio; /* [B] (ACRL_CTRL_MIS)                                    */
 } acrl_controller_desc;
 
 acrl_status acrl_controller_step(const acrl_controller_desc* desc, void* stream);

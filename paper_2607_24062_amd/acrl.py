@@ -21,6 +21,7 @@ ACRL_OK, ACRL_ERR_INVALID_ARG, ACRL_ERR_UNSUPPORTED, ACRL_ERR_WORKSPACE, ACRL_ER
 SCALE_PER_TENSOR, SCALE_PER_ROW, SCALE_MX32 = 0, 1, 2
 ROUND_NEAREST_EVEN, ROUND_TOWARD_ZERO = 0, 1
 Y_GROUP, Y_SEQUENCE, Y_BATCH = 0, 1, 2
+CTRL_ACRL, CTRL_TIS, CTRL_MIS, CTRL_CONTINUOUS, CTRL_FALLBACK = 0, 1, 2, 3, 4
 N_STATS = 10
 STAT_NAMES = ["y_batch", "tok_mean_d", "tok_max_d", "tok_std_d", "mean_h_pi", "mean_h_mu",
               "n_tokens", "n_groups", "tok_mean_logratio", "n_seqs"]
@@ -65,7 +66,8 @@ class ControllerDesc(ctypes.Structure):
                 ("adv", _P), ("adv_per_token", _I32), ("y_level", _I32),
                 ("seq_mean_d", _P), ("group_y", _P), ("stats", _P),
                 ("X", _F32), ("gamma", _F32), ("C", _F32),
-                ("alpha", _P), ("weight", _P)]
+                ("alpha", _P), ("weight", _P), ("mode", _I32), ("k", _F32),
+                ("seq_sum_logratio", _P)]
 
 
 class AcrlError(RuntimeError):
@@ -282,7 +284,8 @@ def acrl_discrepancy_reduce(B: int, L: int, n_groups: int, logp_pi, logp_mu, mas
 # ------------------------------------------------------------------ a8
 def acrl_controller_step(B: int, L: int, n_groups: int, mask, group_of_seq, logp_pi, logp_mu, adv,
                          adv_per_token: bool, y_level: int, seq_mean_d, group_y, stats,
-                         X: float, gamma: float, C: float, want_alpha: bool = True, stream=None):
+                         X: float, gamma: float, C: float, want_alpha: bool = True, stream=None,
+                         mode: int = 0, k: float = 1.0, seq_sum_logratio=None):
     dev = logp_pi.device
     alpha = torch.empty(B * L, dtype=torch.float32, device=dev) if want_alpha else None
     weight = torch.empty(B * L, dtype=torch.float32, device=dev)
@@ -291,7 +294,8 @@ def acrl_controller_step(B: int, L: int, n_groups: int, mask, group_of_seq, logp
                           adv_per_token=int(bool(adv_per_token)), y_level=y_level,
                           seq_mean_d=_ptr(seq_mean_d), group_y=_ptr(group_y), stats=_ptr(stats),
                           X=float(X), gamma=float(gamma), C=float(C), alpha=_ptr(alpha),
-                          weight=_ptr(weight))
+                          weight=_ptr(weight), mode=int(mode), k=float(k),
+                          seq_sum_logratio=_ptr(seq_sum_logratio))
     _check(lib().acrl_controller_step(ctypes.byref(desc), _stream(stream)), "acrl_controller_step")
     return alpha, weight
 

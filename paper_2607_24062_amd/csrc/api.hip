@@ -265,12 +265,18 @@ acrl_status acrl_controller_step(const acrl_controller_desc* d, void* stream) {
   ACRL_REQUIRE(d->C > 1.0f && d->C < 1e30f, "C must be > 1 (got %g)", (double)d->C);
   ACRL_REQUIRE(d->y_level == ACRL_Y_GROUP || d->y_level == ACRL_Y_SEQUENCE || d->y_level == ACRL_Y_BATCH,
                "y_level %d unknown", d->y_level);
+  ACRL_REQUIRE(d->mode >= ACRL_CTRL_ACRL && d->mode <= ACRL_CTRL_FALLBACK, "mode %d unknown", d->mode);
+  if (d->mode == ACRL_CTRL_CONTINUOUS)
+    ACRL_REQUIRE(d->k > 0.0f && d->k < 1e30f, "k must be > 0 (got %g)", (double)d->k);
   if (d->B > 0 && d->L > 0) {
     ACRL_REQUIRE(d->mask && d->logp_pi && d->logp_mu && d->adv && d->weight,
                  "mask, logp_pi, logp_mu, adv and weight are required");
-    if (d->y_level == ACRL_Y_GROUP) ACRL_REQUIRE(d->group_y && d->group_of_seq, "group_y and group_of_seq are required");
-    if (d->y_level == ACRL_Y_SEQUENCE) ACRL_REQUIRE(d->seq_mean_d, "seq_mean_d is required");
-    if (d->y_level == ACRL_Y_BATCH) ACRL_REQUIRE(d->stats, "stats is required");
+    const bool reads_y = d->mode == ACRL_CTRL_ACRL || d->mode == ACRL_CTRL_FALLBACK;
+    if (reads_y && d->y_level == ACRL_Y_GROUP)
+      ACRL_REQUIRE(d->group_y && d->group_of_seq, "group_y and group_of_seq are required");
+    if (reads_y && d->y_level == ACRL_Y_SEQUENCE) ACRL_REQUIRE(d->seq_mean_d, "seq_mean_d is required");
+    if (reads_y && d->y_level == ACRL_Y_BATCH) ACRL_REQUIRE(d->stats, "stats is required");
+    if (d->mode == ACRL_CTRL_MIS) ACRL_REQUIRE(d->seq_sum_logratio, "seq_sum_logratio is required for MIS");
   }
   acrl_status st = acrl::check_device();
   if (st != ACRL_OK) return st;

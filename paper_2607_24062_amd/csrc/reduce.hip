@@ -185,7 +185,10 @@ __global__ __launch_bounds__(kRedThreads) void reduce_batch_kernel(acrl_reduce_d
 }
 
 // Element-wise controller.  alpha and the weight are evaluated in fp64 from
-// the fp32 inputs (exact conversions), then rounded to fp32 once.
+// the fp32 inputs (exact conversions), then rounded to fp32 once.  Modes:
+// Eq. ACRL, token-level TIS (Eq. tis_objective), sequence-level MIS (Eq.
+// mis_objective, from the fp64 per-sequence log-ratio sums of the reduce),
+// and the continuous-reduction / fallback-to-GRPO ablations of Sec. 5.
 __global__ __launch_bounds__(256) void controller_kernel(acrl_controller_desc p) {
   const int64_t n = p.B * p.L;
   const double X = p.X, gamma = p.gamma, lnC = log((double)p.C), C = p.C;
@@ -195,18 +198,40 @@ __global__ __launch_bounds__(256) void controller_kernel(acrl_controller_desc p)
     if (p.mask[t]) {
       const int64_t i = t / p.L;
       const double A = p.adv_per_token ? p.adv[t] : p.adv[i];
-      double Y;
-      if (p.y_level == ACRL_Y_SEQUENCE) Y = p.seq_mean_d[i];
-      else if (p.y_level == ACRL_Y_GROUP) {
-        const int32_t g = p.group_of_seq[i];
-        Y = (g >= 0 && g < p.n_groups) ? (double)p.group_y[g] : __builtin_nan("");
-      }
-      else Y = p.stats[ACRL_STAT_Y_BATCH];
       const double sg = (A > 0) - (A < 0);
-      const double alpha = gamma * sg * (1.0 - Y / X);
-      const double e = alpha * ((double)p.logp_pi[t] - (double)p.logp_mu[t]);  // ln rho
-      a_out = (float)alpha;
-      w_out = (float)(e < lnC ? exp(e) : C);
+      const double lr = (double)p.logp_pi[t] - (double)p.logp_mu[t];  // ln(pi/mu)
+      if (p.mode == ACRL_CTRL_MIS) {
+        const double s = p.seq_sum_logratio[i];  // ln rho_i
+        a_out = 1.0f;
+        w_out = s <= lnC ? (float)exp(s) : 0.0f;
+      } else if (p.mode == ACRL_CTRL_TIS) {
+        a_out = 1.0f;
+        w_out = (float)(lr < lnC ? exp(lr) : C);
+      } else {
+        double alpha;
+        bool grpo = false;
+        if (p.mode == ACRL_CTRL_CONTINUOUS) {
+          alpha = -(double)p.k * sg;
+        } else {
+          double Y;
+          if (p.y_level == ACRL_Y_SEQUENCE) Y = p.seq_mean_d[i];
+          else if (p.y_level == ACRL_Y_GROUP) {
+            const int32_t g = p.group_of_seq[i];
+            Y = (g >= 0 && g < p.n_groups) ? (double)p.group_y[g] : __builtin_nan("");
+          }
+          else Y = p.stats[ACRL_STAT_Y_BATCH];
+          grpo = p.mode == ACRL_CTRL_FALLBACK && Y < X;
+          alpha = gamma * sg * (1.0 - Y / X);
+        }
+        if (grpo) {
+          a_out = 0.0f;
+          w_out = 1.0f;
+        } else {
+          const double e = alpha * lr;  // ln rho
+          a_out = (float)alpha;
+          w_out = (float)(e < lnC ? exp(e) : C);
+        }
+      }
     }
     if (p.alpha) p.alpha[t] = a_out;
     p.weight[t] = w_out;

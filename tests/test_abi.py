@@ -57,7 +57,7 @@ def test_descriptor_layout_matches_binding():
     acrl.lib().acrl_abi_struct_sizes(*[ctypes.byref(s) for s in sizes])
     assert [s.value for s in sizes] == [ctypes.sizeof(acrl.ScoreDesc), ctypes.sizeof(acrl.ReduceDesc),
                                         ctypes.sizeof(acrl.ControllerDesc)]
-    assert acrl.lib().acrl_abi_version() == 1
+    assert acrl.lib().acrl_abi_version() == 2
 
 
 def test_status_strings():

@@ -92,6 +92,47 @@ def test_controller_matches_oracle(level, per_token):
         assert np.all(down(weight) <= np.float32(C))
 
 
+@pytest.mark.parametrize("mode,k", [(oracle.CTRL_TIS, 1.0), (oracle.CTRL_MIS, 1.0),
+                                    (oracle.CTRL_CONTINUOUS, 1.0), (oracle.CTRL_CONTINUOUS, 3.0),
+                                    (oracle.CTRL_FALLBACK, 1.0)])
+def test_controller_modes_match_oracle(mode, k):
+    # TIS (Eq. tis_objective), MIS (Eq. mis_objective), and the continuous-
+    # reduction / fallback-to-GRPO ablations of Sec. 5
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    B, L, ng = 24, 300, 3
+    mask, lp_pi, lp_mu, ent_pi, ent_mu, g = _batch(B, L, ng, 31)
+    red = _gpu_reduce(B, L, ng, mask, lp_pi, lp_mu, ent_pi, ent_mu, g)
+    adv = np.random.default_rng(32).normal(size=B).astype(np.float32)
+    adv[:2] = 0.0
+    t = lambda a: up(torch, dev, np.ascontiguousarray(a).reshape(-1))
+    C = 3.0
+    # MIS keeps a sequence iff its ratio is <= C: leave out sequences whose
+    # log-ratio sum lies within rounding of ln C (none for this seed)
+    near = np.abs(red["seq_sum_logratio"] - math.log(C)) < 1e-6
+    assert not near.any()
+    for X in (float(red["stats"][0]) * 0.5, float(red["stats"][0]) * 2):
+        alpha, weight = acrl.acrl_controller_step(
+            B, L, ng, t(mask), up(torch, dev, g), t(lp_pi), t(lp_mu), t(adv), False, oracle.Y_GROUP,
+            t(red["seq_mean_d"]), t(red["group_y"]), t(red["stats"]), X, 0.65, C, mode=mode, k=k,
+            seq_sum_logratio=up(torch, dev, red["seq_sum_logratio"]))
+        torch.cuda.synchronize()
+        a_ref, w_ref = oracle.controller_step(B, L, mask, g, lp_pi, lp_mu, adv, False, oracle.Y_GROUP,
+                                              red["seq_mean_d"], red["group_y"], red["stats"],
+                                              float(np.float32(X)), float(np.float32(0.65)), C,
+                                              mode=mode, k=float(np.float32(k)))
+        np.testing.assert_allclose(down(alpha), a_ref.astype(np.float32), rtol=2 ** -23, atol=1e-30)
+        # MIS: the GPU sums the fp32 log-ratios in its own order (fp64), the
+        # oracle multiplies the token ratios; elsewhere both round once
+        rtol = 1e-9 * L if mode == oracle.CTRL_MIS else 2 ** -23
+        np.testing.assert_allclose(down(weight), w_ref.astype(np.float32), rtol=max(rtol, 2 ** -23),
+                                   atol=1e-30)
+        assert np.all(down(weight)[mask.reshape(-1) == 0] == 0)
+        if mode == oracle.CTRL_MIS:
+            kept = (red["seq_sum_logratio"] <= math.log(C)).sum()
+            assert 0 < kept < B  # both branches exercised
+
+
 def test_small_workload_end_to_end():
     """quantize -> score -> reduce -> controller on the device against the
     oracle's whole chain on the same seeded inputs."""

@@ -206,3 +206,59 @@ def test_full_size_sampled_rows(name):
     assert (ent >= -1e-4).all() and (ent <= math.log(w.V) + 1e-3).all()
     del h, W, hq, wq, out
     torch.cuda.empty_cache()
+
+
+def test_long_workload_chunked():
+    # Long-response stress workload (4 prompts x 16 rollouts, lengths up to
+    # 16384, per-row FP8): scored in token chunks into the slot layout, checked
+    # on sampled rows against the oracle, then reduced per sequence / group
+    # over the ragged slots and compared with the oracle's reduce of the same
+    # per-token values.
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    w = inputs.WORKLOADS["long"]
+    T = inputs.n_valid(w)
+    slots = inputs.valid_slots(w)
+    assert slots.size == T and w.chunk_rows and T > 4 * w.chunk_rows
+    h = inputs.hidden_bf16_torch(w, T, dev)
+    W = inputs.weights_bf16_torch(w, dev)
+    hq, hs = acrl.acrl_quantize_fp8(h, w.scaling)
+    wq, ws = acrl.acrl_quantize_fp8(W, w.scaling)
+    ids_np = inputs.uniform_ids(w, T)
+    ids = up(torch, dev, ids_np)
+    outs = {k: torch.zeros(w.slots, dtype=torch.float32, device=dev)
+            for k in ("logp_pi", "logp_mu", "entropy_pi", "entropy_mu")}
+    slots_d = up(torch, dev, slots.astype(np.int32))
+    for r0 in range(0, T, w.chunk_rows):
+        r1 = min(T, r0 + w.chunk_rows)
+        acrl.acrl_score_pi_mu(h[r0:r1], W, hq[r0:r1], hs[r0:r1], wq, ws, w.scaling, ids[r0:r1],
+                              inv_temperature=w.inv_temperature, out_slot=slots_d[r0:r1],
+                              n_slots=w.slots, outputs=outs, want=("entropy",))
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.random.default_rng(w.seed).choice(T, 10, replace=False),
+                                     [0, w.chunk_rows - 1, w.chunk_rows, T - 1]]))
+    idx = torch.from_numpy(rows).to(dev)
+    Hs = h.index_select(0, idx).cpu().view(torch.int16).numpy().view(np.uint16)
+    Wb = W.cpu().view(torch.int16).numpy().view(np.uint16)
+    ref = oracle.score(Hs, Wb, down(hq.index_select(0, idx)), down(hs)[rows], down(wq), down(ws),
+                       w.scaling, ids_np[rows], inv_temperature=w.inv_temperature)
+    for tag in ("pi", "mu"):
+        got = down(outs["logp_" + tag])[slots[rows]]
+        assert np.abs(got - ref["logp_" + tag]).max() <= TOL_LOGP
+    # ragged segmented reduce over the whole slot array
+    mask = inputs.mask(w).reshape(-1)
+    groups = inputs.group_of_seq(w)
+    red = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, outs["logp_pi"], outs["logp_mu"],
+                                       up(torch, dev, mask), up(torch, dev, groups),
+                                       entropy_pi=outs["entropy_pi"], entropy_mu=outs["entropy_mu"])
+    torch.cuda.synchronize()
+    lp_pi, lp_mu = down(outs["logp_pi"]), down(outs["logp_mu"])
+    oref = oracle.discrepancy_reduce(w.B, w.L, lp_pi, lp_mu, mask, groups, w.n_prompts,
+                                     ent_pi=down(outs["entropy_pi"]), ent_mu=down(outs["entropy_mu"]))
+    assert np.array_equal(down(red["seq_len"]), oref["seq_len"])
+    n = oref["seq_len"].astype(np.float64)
+    assert (np.abs(down(red["seq_sum_logratio"]) - oref["seq_sum_logratio"]) <= 1e-9 * np.maximum(n, 1)).all()
+    np.testing.assert_allclose(down(red["group_y"]), oref["group_y"], rtol=1e-5, atol=1e-12)
+    assert abs(down(red["stats"])[0] - oref["stats"][0]) <= 1e-5 * abs(oref["stats"][0]) + 1e-12
+    del h, W, hq, wq, outs
+    torch.cuda.empty_cache()
