@@ -88,6 +88,12 @@ def lib() -> ctypes.CDLL:
         L.acrl_ref_controller_step.restype = I32
         L.acrl_ref_controller_step.argtypes = [I64, I64, P, P, P, P, P, I32, I32, P, P, P,
                                                D, D, D, I32, D, P, P]
+        L.acrl_ref_philox4x32_10.restype = None
+        L.acrl_ref_philox4x32_10.argtypes = [P, P, P]
+        L.acrl_ref_sample_uniform.restype = D
+        L.acrl_ref_sample_uniform.argtypes = [ctypes.c_uint64, I64, I64]
+        L.acrl_ref_gumbel_sample.restype = I32
+        L.acrl_ref_gumbel_sample.argtypes = [P, I64, I64, ctypes.c_uint64, I64, P, P]
         L.acrl_ref_reference_x.restype = I32
         L.acrl_ref_reference_x.argtypes = [P, P, I64, P]
         L.acrl_ref_sample_inverse_cdf.restype = I32
@@ -265,3 +271,26 @@ def sample_inverse_cdf(z: np.ndarray, u: np.ndarray) -> np.ndarray:
     ids = np.empty(n_rows, np.int32)
     _check(lib().acrl_ref_sample_inverse_cdf(_p(z), n_rows, V, _p(u), _p(ids)), "sample")
     return ids
+
+
+def philox4x32_10(ctr, key) -> np.ndarray:
+    c = np.ascontiguousarray(ctr, np.uint32)
+    k = np.ascontiguousarray(key, np.uint32)
+    out = np.zeros(4, np.uint32)
+    lib().acrl_ref_philox4x32_10(_p(c), _p(k), _p(out))
+    return out
+
+
+def sample_uniform(seed: int, t: int, v: int) -> float:
+    return float(lib().acrl_ref_sample_uniform(seed, t, v))
+
+
+def gumbel_sample(z: np.ndarray, seed: int, row_offset: int = 0):
+    """Gumbel-max draw from softmax(z) per row; returns (ids, winning keys)."""
+    z = _c(z, np.float64)
+    n_rows, V = z.shape
+    ids = np.empty(n_rows, np.int32)
+    keys = np.empty(n_rows)
+    _check(lib().acrl_ref_gumbel_sample(_p(z), n_rows, V, seed, row_offset, _p(ids), _p(keys)),
+           "gumbel_sample")
+    return ids, keys

@@ -556,3 +556,54 @@ int acrl_ref_sample_inverse_cdf(const double* z, int64_t n_rows, int64_t V,
   }
   return 0;
 }
+
+/* ------------------------------------------------------------------ */
+/* Gumbel-max sampling from mu                                          */
+/* ------------------------------------------------------------------ */
+
+/* Philox4x32-10: each round multiplies words 0 and 2 by the two round
+ * constants, mixes the high halves with the other words and the key, and
+ * the key advances by the two Weyl constants between rounds. */
+void acrl_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u, W0 = 0x9E3779B9u, W1 = 0xBB67AE85u;
+  uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+  uint32_t k0 = key[0], k1 = key[1];
+  for (int round = 0; round < 10; ++round) {
+    const uint64_t p0 = (uint64_t)M0 * c0, p1 = (uint64_t)M1 * c2;
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
+    const uint32_t n0 = hi1 ^ c1 ^ k0, n1 = lo1, n2 = hi0 ^ c3 ^ k1, n3 = lo0;
+    c0 = n0; c1 = n1; c2 = n2; c3 = n3;
+    k0 += W0;
+    k1 += W1;
+  }
+  out[0] = c0; out[1] = c1; out[2] = c2; out[3] = c3;
+}
+
+double acrl_ref_sample_uniform(uint64_t seed, int64_t t, int64_t v) {
+  const uint32_t ctr[4] = {(uint32_t)(v / 4), (uint32_t)t, 0u, 0u};
+  const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  uint32_t w[4];
+  acrl_ref_philox4x32_10(ctr, key, w);
+  return ((double)(w[v % 4] >> 8) + 0.5) / 16777216.0;
+}
+
+int acrl_ref_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t seed,
+                           int64_t row_offset, int32_t* ids, double* key_out) {
+  if (!z || !ids || V <= 0 || n_rows < 0) return -1;
+  for (int64_t r = 0; r < n_rows; ++r) {
+    double best = -INFINITY;
+    int32_t pick = 0;
+    for (int64_t v = 0; v < V; ++v) {
+      const double u = acrl_ref_sample_uniform(seed, row_offset + r, v);
+      const double key = z[r * V + v] - log(-log(u));
+      if (key > best) {
+        best = key;
+        pick = (int32_t)v;
+      }
+    }
+    ids[r] = pick;
+    if (key_out) key_out[r] = best;
+  }
+  return 0;
+}

@@ -135,6 +135,25 @@ int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
 int acrl_ref_reference_x(const double* group_y, const int32_t* group_nseq, int64_t n_groups,
                          double* X);
 
+/* ---- Sampling from mu by the Gumbel-max trick ------------------------ *
+ * Counter-based random numbers: Philox4x32-10 (Salmon, Moraes, Dror, Shaw,
+ * "Parallel random numbers: as easy as 1, 2, 3", SC 2011): 10 rounds on a
+ * 128-bit counter under a 64-bit key.                                       */
+void acrl_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4]);
+
+/* The uniform of vocabulary entry v of token t (global token index) under
+ * seed: word (v mod 4) of Philox4x32-10 on counter (v / 4, t, 0, 0) and key
+ * (seed low 32 bits, seed high 32 bits); u = (word >> 8 + 1/2) 2^-24, in
+ * (0, 1).                                                                    */
+double acrl_ref_sample_uniform(uint64_t seed, int64_t t, int64_t v);
+
+/* Gumbel-max sampling: ids[r] = argmax_v z[r, v] - ln(-ln u(seed, row_offset
+ * + r, v)) over the logits z (natural units, temperature applied); a draw
+ * from softmax(z).  key_out[r] (nullable) = the winning key.  Ties go to the
+ * smaller v.                                                                */
+int acrl_ref_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t seed,
+                           int64_t row_offset, int32_t* ids, double* key_out);
+
 /* ---- fixture helper (not part of the method): inverse-CDF sampling ----- *
  * Samples one id per row from softmax(z_row) using the supplied uniform
  * u[r] in [0,1): the smallest v whose cumulative probability exceeds u.     */
