@@ -585,7 +585,7 @@ double acrl_ref_sample_uniform(uint64_t seed, int64_t t, int64_t v) {
   const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
   uint32_t w[4];
   acrl_ref_philox4x32_10(ctr, key, w);
-  return ((double)(w[v % 4] >> 8) + 0.5) / 16777216.0;
+  return ((double)(w[v % 4] >> 9) + 0.5) / 8388608.0;
 }
 
 int acrl_ref_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t seed,

@@ -143,8 +143,8 @@ void acrl_ref_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32
 
 /* The uniform of vocabulary entry v of token t (global token index) under
  * seed: word (v mod 4) of Philox4x32-10 on counter (v / 4, t, 0, 0) and key
- * (seed low 32 bits, seed high 32 bits); u = (word >> 8 + 1/2) 2^-24, in
- * (0, 1).                                                                    */
+ * (seed low 32 bits, seed high 32 bits); u = (word >> 9 + 1/2) 2^-23, in
+ * (0, 1) and exact in fp32.                                                  */
 double acrl_ref_sample_uniform(uint64_t seed, int64_t t, int64_t v);
 
 /* Gumbel-max sampling: ids[r] = argmax_v z[r, v] - ln(-ln u(seed, row_offset

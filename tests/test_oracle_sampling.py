@@ -40,7 +40,7 @@ def test_uniform_range_and_mean():
     # the four words of one Philox call serve v = 4m .. 4m+3
     w = oracle.philox4x32_10([3, 11, 0, 0], [7, 0])
     for i in range(4):
-        assert oracle.sample_uniform(7, 11, 12 + i) == ((int(w[i]) >> 8) + 0.5) / 2 ** 24
+        assert oracle.sample_uniform(7, 11, 12 + i) == ((int(w[i]) >> 9) + 0.5) / 2 ** 23
 
 
 def test_gumbel_max_draws_from_the_softmax():
