@@ -66,7 +66,6 @@ def main():
     t0 = time.time()
     H = inputs.hidden_bf16_torch(w, T, dev)
     W = inputs.weights_bf16_torch(w, dev)
-    ids = torch.from_numpy(inputs.uniform_ids(w, T)).to(dev)
     slots = torch.from_numpy(inputs.valid_slots(w)).to(dev)
     mask = torch.from_numpy(inputs.mask(w).reshape(-1)).to(dev)
     groups = torch.from_numpy(inputs.group_of_seq(w)).to(dev)
@@ -88,6 +87,17 @@ def main():
     wq_ms = a.elapsed_time(b)
     wq_bytes = V * d * (2 + 1) + (V * d * 2 if w.scaling == inputs.PER_TENSOR else 0)
     log("quantize W: %.3f ms (%.0f GB/s)" % (wq_ms, wq_bytes / wq_ms / 1e6))
+
+    # ---------------- the rollout's tokens: drawn from mu (Gumbel-max in the mu kernel), untimed
+    hq0, hs0 = acrl.acrl_quantize_fp8(H, w.scaling)
+    a.record()
+    ids, _ = acrl.acrl_sample_mu(hq0, hs0, wq, ws, w.scaling, seed=w.seed,
+                                 inv_temperature=w.inv_temperature, want_logp=False)
+    b.record()
+    torch.cuda.synchronize()
+    sample_ms = a.elapsed_time(b)
+    del hq0, hs0
+    log("ids sampled from mu in %.1f ms" % sample_ms)
 
     # ---------------- preallocated step buffers
     hq = torch.empty((T, d), dtype=torch.uint8, device=dev)
@@ -201,8 +211,8 @@ def main():
     # HBM traffic of each score kernel from the committed counter summary, if current
     tr = profiling.load_traffic(os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
                                              "score_%s_traffic.md" % w.name))
-    mu_kernel = "score_kernel<%d>" % {inputs.PER_TENSOR: 1, inputs.PER_ROW: 2, inputs.MX32: 3}[w.scaling]
-    for roof, kname in ((roof_pi, "score_kernel<0>"), (roof_mu, mu_kernel)):
+    mu_kernel = "score_kernel<%d, false>" % {inputs.PER_TENSOR: 1, inputs.PER_ROW: 2, inputs.MX32: 3}[w.scaling]
+    for roof, kname in ((roof_pi, "score_kernel<0, false>"), (roof_mu, mu_kernel)):
         if tr is not None and kname in tr["kernels"]:
             roof["traffic"] = round(tr["kernels"][kname]["traffic_bytes"])
             roof["traffic_unit"] = "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
@@ -225,7 +235,8 @@ def main():
         "dtype": "bf16(pi)+fp8e4m3(mu)",
         "data": "synthetic",
         "config": {"workload": w.describe(), "valid_tokens": T, "slots": w.slots,
-                   "ids": "uniform over the vocabulary (work is id-independent)",
+                   "ids": "drawn from mu at tau (Gumbel-max with Philox4x32-10, seed %d), untimed" % w.seed,
+                   "sample_mu_ms": round(sample_ms, 3),
                    "mfma_frac_combined": round(ideal_ms / ms_per_step, 4),
                    "kernel_ms": {"quantize_h": round(float(t_qh), 4), "pack": round(float(t_pack), 4),
                                  "score_pi": round(float(t_pi), 4),

@@ -93,9 +93,10 @@ enum {
 const char* acrl_status_string(acrl_status status);
 const char* acrl_last_error(void);
 int acrl_abi_version(void);
-/* sizeof of the three descriptor structs as compiled into the library (host);
+/* sizeof of the four descriptor structs as compiled into the library (host);
  * bindings compare them with their own layout.                              */
-void acrl_abi_struct_sizes(size_t* score_desc, size_t* reduce_desc, size_t* controller_desc);
+void acrl_abi_struct_sizes(size_t* score_desc, size_t* reduce_desc, size_t* controller_desc,
+                           size_t* sample_desc);
 
 /* ======================================================================== */
 /* a1/a2  acrl_quantize_fp8 -- FP8 quantization of a bf16 matrix            */
@@ -180,6 +181,40 @@ typedef struct acrl_score_desc {
 acrl_status acrl_score_workspace_size(int64_t n_rows, int64_t d, int64_t V, int mu_scaling,
                                       size_t* bytes);
 acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream);
+
+/* ======================================================================== */
+/* Sampling from mu (the step before scoring: the rollout's token draw)      */
+/* ======================================================================== *
+ * For every row r: a_r = argmax_v [ z_v - ln(-ln u_v) ] with z the mu logits
+ * (as in acrl_score_pi_mu, 1/tau applied) and u_v = (w >> 9 + 1/2) 2^-23,
+ * w = word (v mod 4) of Philox4x32-10 (Salmon et al., SC 2011) on counter
+ * (v / 4, row_offset + r, 0, 0) under key (seed low, seed high 32 bits): the
+ * Gumbel-max trick, i.e. a draw from softmax(z), fused into the mu kernel's
+ * epilogue (the logits never reach memory).  logp_mu[r] (nullable) =
+ * log mu(a_r).  The draw depends only on (seed, row_offset + r), so chunked
+ * calls reproduce one call.
+ * Requirements: as acrl_score_pi_mu for n_rows, d, V, mu_scaling and the
+ * operands; workspace of acrl_score_workspace_size() bytes.
+ */
+typedef struct acrl_sample_desc {
+  int64_t n_rows;
+  int64_t d;
+  int64_t V;
+  const void* hq;               /* e4m3 [n_rows, d]                                         */
+  const void* hq_scales;
+  const void* wq;               /* e4m3 [V, d]                                              */
+  const void* wq_scales;
+  int32_t mu_scaling;
+  float inv_temperature;        /* 1/tau (> 0)                                              */
+  uint64_t seed;
+  int64_t row_offset;           /* global token index of row 0 (>= 0)                       */
+  int32_t* ids;                 /* [n_rows] out: sampled vocabulary rows                    */
+  float* logp_mu;               /* [n_rows] out, nullable                                   */
+  void* workspace;
+  size_t workspace_bytes;
+} acrl_sample_desc;
+
+acrl_status acrl_sample_mu(const acrl_sample_desc* desc, void* stream);
 
 /* Tracing hook (observability, per calling thread).  With n == 4, every later
  * acrl_score_pi_mu call of this thread records the caller-owned hipEvent_t

@@ -31,7 +31,7 @@ EXPORTED = [
     "acrl_quantize_workspace_size", "acrl_quantize_fp8", "acrl_fp8_encode",
     "acrl_score_workspace_size", "acrl_score_pi_mu", "acrl_trace_score_events",
     "acrl_reduce_workspace_size", "acrl_discrepancy_reduce",
-    "acrl_controller_step", "acrl_reference_from_groups",
+    "acrl_controller_step", "acrl_reference_from_groups", "acrl_sample_mu",
 ]
 
 _P = ctypes.c_void_p
@@ -70,6 +70,14 @@ class ControllerDesc(ctypes.Structure):
                 ("seq_sum_logratio", _P)]
 
 
+class SampleDesc(ctypes.Structure):
+    _fields_ = [("n_rows", _I64), ("d", _I64), ("V", _I64),
+                ("hq", _P), ("hq_scales", _P), ("wq", _P), ("wq_scales", _P),
+                ("mu_scaling", _I32), ("inv_temperature", _F32),
+                ("seed", ctypes.c_uint64), ("row_offset", _I64),
+                ("ids", _P), ("logp_mu", _P), ("workspace", _P), ("workspace_bytes", _SZ)]
+
+
 class AcrlError(RuntimeError):
     def __init__(self, status: int, where: str, detail: str):
         super().__init__("%s failed: %s (%s)" % (where, _status_names.get(status, status), detail))
@@ -96,7 +104,7 @@ def lib() -> ctypes.CDLL:
         L.acrl_last_error.argtypes = []
         L.acrl_abi_version.restype = _I32
         L.acrl_abi_struct_sizes.restype = None
-        L.acrl_abi_struct_sizes.argtypes = [ctypes.POINTER(_SZ)] * 3
+        L.acrl_abi_struct_sizes.argtypes = [ctypes.POINTER(_SZ)] * 4
         L.acrl_quantize_workspace_size.restype = _I32
         L.acrl_quantize_workspace_size.argtypes = [_I64, _I64, _I32, ctypes.POINTER(_SZ)]
         L.acrl_quantize_fp8.restype = _I32
@@ -117,9 +125,12 @@ def lib() -> ctypes.CDLL:
         L.acrl_controller_step.argtypes = [ctypes.POINTER(ControllerDesc), _P]
         L.acrl_reference_from_groups.restype = _I32
         L.acrl_reference_from_groups.argtypes = [_P, _P, _I64, ctypes.POINTER(_F32)]
-        sizes = [_SZ(), _SZ(), _SZ()]
+        L.acrl_sample_mu.restype = _I32
+        L.acrl_sample_mu.argtypes = [ctypes.POINTER(SampleDesc), _P]
+        sizes = [_SZ(), _SZ(), _SZ(), _SZ()]
         L.acrl_abi_struct_sizes(*[ctypes.byref(s) for s in sizes])
-        want = [ctypes.sizeof(ScoreDesc), ctypes.sizeof(ReduceDesc), ctypes.sizeof(ControllerDesc)]
+        want = [ctypes.sizeof(ScoreDesc), ctypes.sizeof(ReduceDesc), ctypes.sizeof(ControllerDesc),
+                ctypes.sizeof(SampleDesc)]
         got = [s.value for s in sizes]
         if got != want:
             raise RuntimeError("libacrl descriptor layout mismatch: library %s, binding %s" % (got, want))
@@ -239,6 +250,34 @@ def acrl_score_pi_mu(h, w, hq, hq_scales, wq, wq_scales, mu_scaling: int, token_
                      error_flag=_ptr(error_flag), workspace=_ptr(ws), workspace_bytes=nb.value)
     _check(lib().acrl_score_pi_mu(ctypes.byref(desc), _stream(stream)), "acrl_score_pi_mu")
     return out
+
+
+def acrl_sample_mu(hq, hq_scales, wq, wq_scales, mu_scaling: int, seed: int, row_offset: int = 0,
+                   inv_temperature: float = 1.0, ids=None, logp_mu=None, want_logp: bool = True,
+                   stream=None):
+    """Draw one token per row of hq from mu (Gumbel-max in the mu kernel).
+
+    Returns (ids int32 [n_rows], logp_mu float32 [n_rows] or None)."""
+    _dev(hq, torch.uint8, "hq")
+    _dev(wq, torch.uint8, "wq")
+    n_rows, d = hq.shape
+    V = wq.shape[0]
+    dev = hq.device
+    if ids is None:
+        ids = torch.empty(n_rows, dtype=torch.int32, device=dev)
+    if logp_mu is None and want_logp:
+        logp_mu = torch.empty(n_rows, dtype=torch.float32, device=dev)
+    nb = _SZ()
+    _check(lib().acrl_score_workspace_size(n_rows, d, V, mu_scaling, ctypes.byref(nb)),
+           "acrl_score_workspace_size")
+    ws = _workspace(nb.value, dev)
+    desc = SampleDesc(n_rows=n_rows, d=d, V=V, hq=_ptr(hq), hq_scales=_ptr(hq_scales), wq=_ptr(wq),
+                      wq_scales=_ptr(wq_scales), mu_scaling=mu_scaling,
+                      inv_temperature=float(inv_temperature), seed=int(seed) & (2 ** 64 - 1),
+                      row_offset=int(row_offset), ids=_ptr(ids), logp_mu=_ptr(logp_mu),
+                      workspace=_ptr(ws), workspace_bytes=nb.value)
+    _check(lib().acrl_sample_mu(ctypes.byref(desc), _stream(stream)), "acrl_sample_mu")
+    return ids, logp_mu
 
 
 def acrl_trace_score_events(events) -> None:

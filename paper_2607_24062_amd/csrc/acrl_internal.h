@@ -33,12 +33,14 @@ struct ScorePlan {
   size_t ws_part_offset[2];  // byte offsets of the (M, S, U) partials of pi / mu
   size_t ws_logit_offset[2]; // byte offsets of the sampled-token logits of pi / mu
   size_t ws_pack_offset[4];  // byte offsets of the packed W, H (bf16) and Wq, Hq (e4m3)
+  size_t ws_best_offset;     // sampling: the strips' best key, logit and row
   size_t ws_bytes;
 };
 ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V);
 // Events recorded around the score kernels (tracing hook), per thread.
 void set_score_trace(void* const* events, int n);
 hipError_t launch_score(const acrl_score_desc& desc, const ScorePlan& plan, hipStream_t s);
+hipError_t launch_sample(const acrl_sample_desc& desc, const ScorePlan& plan, hipStream_t s);
 
 size_t reduce_workspace_bytes(int64_t B, int64_t L, int64_t n_groups);
 hipError_t launch_reduce(const acrl_reduce_desc& desc, hipStream_t s);

@@ -142,10 +142,12 @@ const char* acrl_last_error(void) { return acrl::g_last_error; }
 
 int acrl_abi_version(void) { return ACRL_ABI_VERSION; }
 
-void acrl_abi_struct_sizes(size_t* score_desc, size_t* reduce_desc, size_t* controller_desc) {
+void acrl_abi_struct_sizes(size_t* score_desc, size_t* reduce_desc, size_t* controller_desc,
+                           size_t* sample_desc) {
   if (score_desc) *score_desc = sizeof(acrl_score_desc);
   if (reduce_desc) *reduce_desc = sizeof(acrl_reduce_desc);
   if (controller_desc) *controller_desc = sizeof(acrl_controller_desc);
+  if (sample_desc) *sample_desc = sizeof(acrl_sample_desc);
 }
 
 acrl_status acrl_quantize_workspace_size(int64_t rows, int64_t cols, int scaling, size_t* bytes) {
@@ -225,6 +227,40 @@ acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream) {
   st = acrl::check_device();
   if (st != ACRL_OK) return st;
   return acrl::hip_status(acrl::launch_score(*desc, plan, (hipStream_t)stream), "acrl_score_pi_mu launch");
+}
+
+acrl_status acrl_sample_mu(const acrl_sample_desc* d, void* stream) {
+  ACRL_REQUIRE(d, "desc is NULL");
+  ACRL_REQUIRE(d->n_rows >= 0 && d->n_rows < (int64_t)INT32_MAX - 512, "n_rows %lld out of range",
+               (long long)d->n_rows);
+  ACRL_REQUIRE(d->d > 0 && d->d % 128 == 0, "d = %lld must be a positive multiple of 128", (long long)d->d);
+  ACRL_REQUIRE(d->V > 0 && d->V < (int64_t)INT32_MAX - 512, "V = %lld out of range", (long long)d->V);
+  ACRL_REQUIRE(acrl::score_size_ok(d->V, d->d) && acrl::score_size_ok(d->n_rows, d->d), "rows x d too large");
+  ACRL_REQUIRE(d->mu_scaling == ACRL_SCALE_PER_TENSOR || d->mu_scaling == ACRL_SCALE_PER_ROW ||
+                   d->mu_scaling == ACRL_SCALE_MX32,
+               "mu_scaling %d unknown", d->mu_scaling);
+  ACRL_REQUIRE(d->inv_temperature > 0.0f && d->inv_temperature < 1e30f,
+               "inv_temperature must be positive and finite");
+  ACRL_REQUIRE(d->row_offset >= 0 && d->row_offset + d->n_rows <= ((int64_t)1 << 32),
+               "row_offset + n_rows must lie in [0, 2^32] (the generator's token counter)");
+  ACRL_REQUIRE(d->wq && d->wq_scales, "wq and wq_scales are required");
+  ACRL_REQUIRE(acrl::aligned16(d->wq) && acrl::aligned16(d->wq_scales), "wq and wq_scales must be 16-byte aligned");
+  if (d->n_rows > 0) {
+    ACRL_REQUIRE(d->hq && d->hq_scales && d->ids, "hq, hq_scales and ids are required");
+    ACRL_REQUIRE(acrl::aligned16(d->hq) && acrl::aligned16(d->hq_scales), "hq and hq_scales must be 16-byte aligned");
+  }
+  const acrl::ScorePlan plan = acrl::plan_score(d->n_rows, d->d, d->V);
+  if (d->n_rows > 0 && (!d->workspace || d->workspace_bytes < plan.ws_bytes)) {
+    set_error("acrl_sample_mu needs %zu workspace bytes, got %zu", plan.ws_bytes, d->workspace_bytes);
+    return ACRL_ERR_WORKSPACE;
+  }
+  if (d->n_rows > 0 && !acrl::aligned16(d->workspace)) {
+    set_error("workspace must be 16-byte aligned");
+    return ACRL_ERR_INVALID_ARG;
+  }
+  acrl_status st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(acrl::launch_sample(*d, plan, (hipStream_t)stream), "acrl_sample_mu launch");
 }
 
 acrl_status acrl_trace_score_events(void* const* events, int n) {

@@ -75,7 +75,37 @@ struct ScoreParams {
   const int32_t* ids;
   float* part;             // [3][n_strips][n_rows]: M, S, U of each strip
   float* logit;            // [n_rows]: z[a_t] (natural units)
+  // sampling (Gumbel-max) only
+  uint32_t seed_lo, seed_hi;
+  int64_t row_offset;      // global token index of row 0 (the generator's counter)
+  float* best_key;         // [n_strips][n_rows]: the strip's largest Gumbel key (log2 units)
+  float* best_logit;       // [n_strips][n_rows]: its logit (natural units)
+  int32_t* best_id;        // [n_strips][n_rows]: its vocabulary row
 };
+
+// Philox4x32-10 (Salmon et al., SC 2011): 10 rounds on a 128-bit counter
+// under a 64-bit key; each round multiplies words 0 and 2 by the round
+// constants and mixes the high halves with the other words and the key, the
+// key advancing by the Weyl constants.
+__device__ __forceinline__ void philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2, uint32_t c3, uint32_t k0,
+                                              uint32_t k1, uint32_t (&out)[4]) {
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c0), lo0 = 0xD2511F53u * c0;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c2), lo1 = 0xCD9E8D57u * c2;
+    const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
+    c0 = n0;
+    c1 = lo1;
+    c2 = n2;
+    c3 = lo0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  out[0] = c0;
+  out[1] = c1;
+  out[2] = c2;
+  out[3] = c3;
+}
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
@@ -170,7 +200,7 @@ struct Pipe {
   static constexpr int kLoadsPerChunk = (MODE == kMX) ? 10 : 8;  // per wave, at least
 };
 
-template <int MODE>
+template <int MODE, bool SAMPLE>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void score_kernel(ScoreParams p) {
   constexpr int NS = Pipe<MODE>::kStages;
@@ -205,11 +235,16 @@ void score_kernel(ScoreParams p) {
   int tok[4], id[4];
   float c2[4], cz[4];
   float M[4], S[4], U[4];
+  float bk[4], bz[4];  // sampling: best Gumbel key of the lane and its logit
+  int bi[4];           //           and vocabulary row
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     tok[j] = t0 + wt * 128 + j * 32 + r32;
     const int tc = min(tok[j], p.n_rows - 1);
-    id[j] = p.ids[tc];
+    id[j] = SAMPLE ? -1 : p.ids[tc];
+    bk[j] = -INFINITY;
+    bz[j] = 0.0f;
+    bi[j] = 0;
     float ct = p.inv_temp;
     if constexpr (MODE == kFP8Row) ct *= p.b_scale[tc];
     if constexpr (MODE == kFP8Tensor) ct *= p.b_scale[0] * p.a_scale[0];
@@ -445,6 +480,31 @@ void score_kernel(ScoreParams p) {
           // finish the update here, ahead of the branch below: otherwise the
           // pass is sunk past it and the values of all 16 blocks stay live
           asm volatile("" : "+v"(M[j]), "+v"(S[j]), "+v"(U[j]));
+          if constexpr (SAMPLE) {
+            // Gumbel-max: key = y - log2(-log2 u), a monotone map of
+            // z - ln(-ln u); u from Philox on counter (v / 4, token, 0, 0),
+            // one call per 4 consecutive rows
+            const uint32_t tokg = (uint32_t)(p.row_offset + tok[j]);
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) {
+              const int vb = v0 + 32 * b + 8 * q4 + 4 * g;  // multiple of 4
+              uint32_t w4[4];
+              philox4x32_10((uint32_t)vb >> 2, tokg, 0u, 0u, p.seed_lo, p.seed_hi, w4);
+#pragma unroll
+              for (int ii = 0; ii < 4; ++ii) {
+                const int i = 4 * q4 + ii;
+                const float u = ((float)(w4[ii] >> 9) + 0.5f) * 0x1p-23f;
+                float key = fmaf(v[i], c2[j], -__builtin_amdgcn_logf(-__builtin_amdgcn_logf(u)));
+                if constexpr (kTail) key = (nv - (float)(16 * b + i)) > 0.0f ? key : -INFINITY;
+                if (key > bk[j]) {
+                  bk[j] = key;
+                  bz[j] = v[i] * cz[j];
+                  bi[j] = vb + ii;
+                }
+              }
+              __builtin_amdgcn_sched_barrier(0);  // one generator call live at a time
+            }
+          }
           // the sampled token a_t: rare branch, taken by the one lane holding it
           const int rel = id[j] - v0;
           if ((unsigned)rel < 128u && (rel >> 5) == b && ((rel >> 2) & 1) == g) {
@@ -594,19 +654,38 @@ void score_kernel(ScoreParams p) {
   __syncthreads();  // every wave is done with the stages before LDS is reused
 
   // ---- merge the lane pair (l, l^32), then the two vocabulary halves
+  // (sampling: the larger key wins, the smaller row on a tie)
+  auto take_best = [](float& k, float& z, int& i, float k2, float z2, int i2) {
+    if (k2 > k || (k2 == k && i2 < i)) {
+      k = k2;
+      z = z2;
+      i = i2;
+    }
+  };
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const float M2 = __shfl_xor(M[j], 32), S2 = __shfl_xor(S[j], 32), U2 = __shfl_xor(U[j], 32);
     merge_state(M[j], S[j], U[j], M2, S2, U2);
+    if constexpr (SAMPLE) {
+      const float k2 = __shfl_xor(bk[j], 32), z2 = __shfl_xor(bz[j], 32);
+      const int i2 = __shfl_xor(bi[j], 32);
+      take_best(bk[j], bz[j], bi[j], k2, z2, i2);
+    }
   }
+  constexpr int XS = SAMPLE ? 6 : 3;  // floats exchanged per token
   float* xch = reinterpret_cast<float*>(lds);  // LDS is free after the last barrier
   if (wv == 1 && g == 0) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int k = wt * 128 + j * 32 + r32;
-      xch[3 * k + 0] = M[j];
-      xch[3 * k + 1] = S[j];
-      xch[3 * k + 2] = U[j];
+      xch[XS * k + 0] = M[j];
+      xch[XS * k + 1] = S[j];
+      xch[XS * k + 2] = U[j];
+      if constexpr (SAMPLE) {
+        xch[XS * k + 3] = bk[j];
+        xch[XS * k + 4] = bz[j];
+        xch[XS * k + 5] = __int_as_float(bi[j]);
+      }
     }
   }
   __syncthreads();
@@ -615,12 +694,19 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int k = wt * 128 + j * 32 + r32;
-      merge_state(M[j], S[j], U[j], xch[3 * k + 0], xch[3 * k + 1], xch[3 * k + 2]);
+      merge_state(M[j], S[j], U[j], xch[XS * k + 0], xch[XS * k + 1], xch[XS * k + 2]);
+      if constexpr (SAMPLE)
+        take_best(bk[j], bz[j], bi[j], xch[XS * k + 3], xch[XS * k + 4], __float_as_int(xch[XS * k + 5]));
       if (tok[j] < p.n_rows) {
         const int64_t o = (int64_t)st * p.n_rows + tok[j];
         p.part[o] = M[j];
         p.part[plane + o] = S[j];
         p.part[2 * plane + o] = U[j];
+        if constexpr (SAMPLE) {
+          p.best_key[o] = bk[j];
+          p.best_logit[o] = bz[j];
+          p.best_id[o] = bi[j];
+        }
       }
     }
   }
@@ -696,6 +782,42 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams p) {
   }
 }
 
+struct SampleMergeParams {
+  int n_rows;
+  int n_strips;
+  const float* part;
+  const float* best_key;
+  const float* best_logit;
+  const int32_t* best_id;
+  int32_t* ids;
+  float* logp;
+};
+
+// One thread per row: the sampled row is the strips' best Gumbel key (the
+// smaller row on a tie); its log-probability is its logit minus the merged
+// log-sum-exp.
+__global__ __launch_bounds__(256) void sample_merge_kernel(SampleMergeParams p) {
+  const int r = blockIdx.x * blockDim.x + threadIdx.x;
+  if (r >= p.n_rows) return;
+  const int64_t plane = (int64_t)p.n_strips * p.n_rows;
+  float M = kInitMax, S = 0.f, U = 0.f;
+  float bk = -INFINITY, bz = 0.f;
+  int bi = 0;
+  for (int s = 0; s < p.n_strips; ++s) {
+    const int64_t o = (int64_t)s * p.n_rows + r;
+    merge_state(M, S, U, p.part[o], p.part[plane + o], p.part[2 * plane + o]);
+    const float k = p.best_key[o];
+    const int i = p.best_id[o];
+    if (k > bk || (k == bk && i < bi)) {
+      bk = k;
+      bz = p.best_logit[o];
+      bi = i;
+    }
+  }
+  p.ids[r] = bi;
+  if (p.logp) p.logp[r] = bz - (M + log2f(S)) * kLn2;
+}
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 thread_local hipEvent_t g_trace[4];
@@ -756,6 +878,9 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V) {
     pl.ws_logit_offset[q] = off;
     off += logit_bytes;
   }
+  // sampling: the strips' best Gumbel key, its logit and row
+  pl.ws_best_offset = off;
+  off += 3 * align_up((size_t)pl.n_strips * (size_t)n_rows * sizeof(float), 256);
   // packed operands: W, H (2d bytes per row), Wq, Hq (d bytes per row)
   const size_t vrows = (size_t)pl.n_vtiles * kTileV, trows = (size_t)pl.n_ttiles * kTileT;
   const size_t pack_bytes[4] = {vrows * 2 * (size_t)d, trows * 2 * (size_t)d, vrows * (size_t)d, trows * (size_t)d};
@@ -803,7 +928,7 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   pp.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[0]);
   pp.logit = reinterpret_cast<float*>(ws + pl.ws_logit_offset[0]);
   trace(0, s);
-  hipLaunchKernelGGL(score_kernel<kBF16>, dim3(grid), dim3(kThreads), 0, s, pp);
+  hipLaunchKernelGGL((score_kernel<kBF16, false>), dim3(grid), dim3(kThreads), 0, s, pp);
   trace(1, s);
 
   // mu: e4m3 operands
@@ -816,14 +941,14 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
     pm.a_mx = static_cast<const uint8_t*>(dsc.wq_scales);
     pm.b_mx = static_cast<const uint8_t*>(dsc.hq_scales);
-    hipLaunchKernelGGL(score_kernel<kMX>, dim3(grid), dim3(kThreads), 0, s, pm);
+    hipLaunchKernelGGL((score_kernel<kMX, false>), dim3(grid), dim3(kThreads), 0, s, pm);
   } else {
     pm.a_scale = static_cast<const float*>(dsc.wq_scales);
     pm.b_scale = static_cast<const float*>(dsc.hq_scales);
     if (dsc.mu_scaling == ACRL_SCALE_PER_ROW)
-      hipLaunchKernelGGL(score_kernel<kFP8Row>, dim3(grid), dim3(kThreads), 0, s, pm);
+      hipLaunchKernelGGL((score_kernel<kFP8Row, false>), dim3(grid), dim3(kThreads), 0, s, pm);
     else
-      hipLaunchKernelGGL(score_kernel<kFP8Tensor>, dim3(grid), dim3(kThreads), 0, s, pm);
+      hipLaunchKernelGGL((score_kernel<kFP8Tensor, false>), dim3(grid), dim3(kThreads), 0, s, pm);
   }
 
   trace(2, s);
@@ -845,6 +970,65 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   mp.error_flag = dsc.error_flag;
   hipLaunchKernelGGL(merge_kernel, dim3((unsigned)((dsc.n_rows + 255) / 256)), dim3(256), 0, s, mp);
   trace(3, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_sample(const acrl_sample_desc& dsc, const ScorePlan& pl, hipStream_t s) {
+  if (dsc.n_rows == 0) return hipSuccess;
+  uint8_t* ws = static_cast<uint8_t*>(dsc.workspace);
+  const void* srcs[2] = {dsc.wq, dsc.hq};
+  const int64_t src_rows[2] = {dsc.V, dsc.n_rows};
+  const int64_t src_tiles[2] = {pl.n_vtiles, pl.n_ttiles};
+  for (int q = 0; q < 2; ++q) {
+    const int64_t units = src_tiles[q] * kTileV * (dsc.d / 16);
+    const unsigned blocks = (unsigned)std::min<int64_t>((units + 255) / 256, 8192);
+    hipLaunchKernelGGL(pack_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint8_t*>(srcs[q]),
+                       (uint32_t)src_rows[q], (uint32_t)dsc.d, (uint32_t)units, ws + pl.ws_pack_offset[2 + q]);
+  }
+  ScoreParams pm{};
+  pm.V = (int)dsc.V;
+  pm.n_rows = (int)dsc.n_rows;
+  pm.n_vtiles = pl.n_vtiles;
+  pm.tiles_per_strip = pl.tiles_per_strip;
+  pm.n_strips = pl.n_strips;
+  pm.n_ttiles = pl.n_ttiles;
+  pm.n_tblocks = pl.n_tblocks;
+  pm.inv_temp = dsc.inv_temperature;
+  pm.mx_row_bytes = (int)(dsc.d / 32);
+  pm.a = ws + pl.ws_pack_offset[2];
+  pm.b = ws + pl.ws_pack_offset[3];
+  pm.n_chunks = (int)(dsc.d / kChunk);
+  pm.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[1]);
+  pm.seed_lo = (uint32_t)dsc.seed;
+  pm.seed_hi = (uint32_t)(dsc.seed >> 32);
+  pm.row_offset = dsc.row_offset;
+  const size_t best_plane = align_up((size_t)pl.n_strips * (size_t)dsc.n_rows * sizeof(float), 256);
+  pm.best_key = reinterpret_cast<float*>(ws + pl.ws_best_offset);
+  pm.best_logit = reinterpret_cast<float*>(ws + pl.ws_best_offset + best_plane);
+  pm.best_id = reinterpret_cast<int32_t*>(ws + pl.ws_best_offset + 2 * best_plane);
+  const unsigned grid = (unsigned)pl.grid;
+  if (dsc.mu_scaling == ACRL_SCALE_MX32) {
+    pm.a_mx = static_cast<const uint8_t*>(dsc.wq_scales);
+    pm.b_mx = static_cast<const uint8_t*>(dsc.hq_scales);
+    hipLaunchKernelGGL((score_kernel<kMX, true>), dim3(grid), dim3(kThreads), 0, s, pm);
+  } else {
+    pm.a_scale = static_cast<const float*>(dsc.wq_scales);
+    pm.b_scale = static_cast<const float*>(dsc.hq_scales);
+    if (dsc.mu_scaling == ACRL_SCALE_PER_ROW)
+      hipLaunchKernelGGL((score_kernel<kFP8Row, true>), dim3(grid), dim3(kThreads), 0, s, pm);
+    else
+      hipLaunchKernelGGL((score_kernel<kFP8Tensor, true>), dim3(grid), dim3(kThreads), 0, s, pm);
+  }
+  SampleMergeParams mp{};
+  mp.n_rows = (int)dsc.n_rows;
+  mp.n_strips = pl.n_strips;
+  mp.part = pm.part;
+  mp.best_key = pm.best_key;
+  mp.best_logit = pm.best_logit;
+  mp.best_id = pm.best_id;
+  mp.ids = dsc.ids;
+  mp.logp = dsc.logp_mu;
+  hipLaunchKernelGGL(sample_merge_kernel, dim3((unsigned)((dsc.n_rows + 255) / 256)), dim3(256), 0, s, mp);
   return hipGetLastError();
 }
 

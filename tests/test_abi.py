@@ -53,10 +53,10 @@ def test_exported_dynamic_symbols_match_header():
 
 def test_descriptor_layout_matches_binding():
     acrl = _acrl()
-    sizes = [ctypes.c_size_t() for _ in range(3)]
+    sizes = [ctypes.c_size_t() for _ in range(4)]
     acrl.lib().acrl_abi_struct_sizes(*[ctypes.byref(s) for s in sizes])
     assert [s.value for s in sizes] == [ctypes.sizeof(acrl.ScoreDesc), ctypes.sizeof(acrl.ReduceDesc),
-                                        ctypes.sizeof(acrl.ControllerDesc)]
+                                        ctypes.sizeof(acrl.ControllerDesc), ctypes.sizeof(acrl.SampleDesc)]
     assert acrl.lib().acrl_abi_version() == 2
 
 

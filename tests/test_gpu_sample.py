@@ -1,0 +1,86 @@
+"""GPU parity of acrl_sample_mu (Gumbel-max draw from mu, fused into the mu
+kernel) with the oracle's Gumbel-max sampler on the same counter-based
+uniforms (Philox4x32-10).
+
+Where floating point decides the argmax, the kernel's fp32 logits and
+hardware log2 may pick a different row than the oracle's fp64 keys when the
+two best keys are within rounding: the drawn row must then be within that
+rounding of the oracle's best key, and rows whose best key clears the
+runner-up by more than it must match exactly.  The sampled log-prob is
+checked like the scorer's (2e-3)."""
+import numpy as np
+import pytest
+
+import inputs
+import oracle
+from cases import TOL_LOGP, random_bf16
+from gpu_util import down, torch_dev, up, up_bf16
+
+pytestmark = pytest.mark.gpu
+
+KEY_TOL = 2e-3  # fp32 logits (~1e-5 relative) and the hardware log2 against fp64
+
+
+def _oracle_keys(z, seed, row_offset):
+    n, V = z.shape
+    u = np.array([[oracle.sample_uniform(seed, row_offset + r, v) for v in range(V)] for r in range(n)])
+    return z - np.log(-np.log(u))
+
+
+@pytest.mark.parametrize("scaling", [oracle.PER_ROW, oracle.PER_TENSOR, oracle.MX32])
+@pytest.mark.parametrize("T,V,d,inv_temp", [(300, 1000, 256, 1.0), (65, 300, 128, 1 / 0.7)])
+def test_sample_matches_oracle(scaling, T, V, d, inv_temp):
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    H = random_bf16((T, d), 41 + T)
+    W = random_bf16((V, d), 42 + V, std=2.5 / np.sqrt(d))
+    h, w = up_bf16(torch, dev, H), up_bf16(torch, dev, W)
+    hq, hs = acrl.acrl_quantize_fp8(h, scaling)
+    wq, ws = acrl.acrl_quantize_fp8(w, scaling)
+    seed, off = 0x1234_5678_9ABC, 1000
+    ids, lp = acrl.acrl_sample_mu(hq, hs, wq, ws, scaling, seed, row_offset=off, inv_temperature=inv_temp)
+    torch.cuda.synchronize()
+    ids, lp = down(ids), down(lp)
+    assert ((ids >= 0) & (ids < V)).all()
+    z = np.stack([oracle.logits_mu(down(hq)[r], oracle._row_scale(down(hs), scaling, r), down(wq),
+                                   down(ws), scaling, inv_temp) for r in range(T)])
+    keys = _oracle_keys(z, seed, off)
+    best = keys.max(axis=1)
+    srt = np.sort(keys, axis=1)
+    clear = srt[:, -1] - srt[:, -2] > KEY_TOL
+    want = keys.argmax(axis=1)
+    assert (keys[np.arange(T), ids] >= best - KEY_TOL).all()
+    assert np.array_equal(ids[clear], want[clear])
+    assert clear.mean() > 0.9
+    # log mu of the drawn row
+    lse = np.log(np.exp(z - z.max(axis=1, keepdims=True)).sum(axis=1)) + z.max(axis=1)
+    np.testing.assert_allclose(lp, z[np.arange(T), ids] - lse, atol=TOL_LOGP, rtol=0)
+
+
+def test_sample_chunked_equals_one_shot_and_frequencies():
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    T, V, d = 4096, 64, 128
+    H = random_bf16((T, d), 5)
+    W = random_bf16((V, d), 6, std=0.3)
+    # every row the same hidden state: the draws are iid from one softmax
+    H[:] = H[0]
+    h, w = up_bf16(torch, dev, H), up_bf16(torch, dev, W)
+    hq, hs = acrl.acrl_quantize_fp8(h, oracle.PER_ROW)
+    wq, ws = acrl.acrl_quantize_fp8(w, oracle.PER_ROW)
+    a, _ = acrl.acrl_sample_mu(hq, hs, wq, ws, oracle.PER_ROW, 99)
+    b = torch.empty_like(a)
+    for r0 in range(0, T, 1000):
+        r1 = min(T, r0 + 1000)
+        acrl.acrl_sample_mu(hq[r0:r1], hs[r0:r1], wq, ws, oracle.PER_ROW, 99, row_offset=r0, ids=b[r0:r1],
+                            want_logp=False)
+    torch.cuda.synchronize()
+    a, b = down(a), down(b)
+    assert np.array_equal(a, b)
+    z = oracle.logits_mu(down(hq)[0], oracle._row_scale(down(hs), oracle.PER_ROW, 0), down(wq), down(ws),
+                         oracle.PER_ROW, 1.0)
+    p = np.exp(z - z.max())
+    p /= p.sum()
+    freq = np.bincount(a, minlength=V) / T
+    sigma = np.sqrt(p * (1 - p) / T)
+    assert (np.abs(freq - p) < 5 * sigma + 1e-9).all()
