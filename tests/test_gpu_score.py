@@ -262,3 +262,27 @@ def test_long_workload_chunked():
     assert abs(down(red["stats"])[0] - oref["stats"][0]) <= 1e-5 * abs(oref["stats"][0]) + 1e-12
     del h, W, hq, wq, outs
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("scaling", [oracle.PER_ROW, oracle.PER_TENSOR, oracle.MX32])
+def test_truncated_fp8_end_to_end(scaling):
+    # the stress test's Q(x) = trunc(x/S) (Sec. 5.3): mu quantized toward
+    # zero on the GPU, bit-exact with the oracle's quantizer, then scored
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    T, V, d = 300, 1100, 256
+    H = random_bf16((T, d), 71)
+    W = random_bf16((V, d), 72, std=2.5 / 16)
+    h, w = up_bf16(torch, dev, H), up_bf16(torch, dev, W)
+    hq, hs = acrl.acrl_quantize_fp8(h, scaling, rounding=acrl.ROUND_TOWARD_ZERO)
+    wq, ws = acrl.acrl_quantize_fp8(w, scaling, rounding=acrl.ROUND_TOWARD_ZERO)
+    hq_o, hs_o = oracle.quantize_fp8(H, scaling, rounding=oracle.ROUND_TOWARD_ZERO)
+    wq_o, ws_o = oracle.quantize_fp8(W, scaling, rounding=oracle.ROUND_TOWARD_ZERO)
+    assert np.array_equal(down(hq), hq_o) and np.array_equal(down(wq), wq_o)
+    assert np.array_equal(down(hs).view(np.uint8), hs_o.view(np.uint8))
+    ids = np.random.default_rng(73).integers(0, V, size=T).astype(np.int32)
+    out = acrl.acrl_score_pi_mu(h, w, hq, hs, wq, ws, scaling, up(torch, dev, ids))
+    torch.cuda.synchronize()
+    res = {k: down(v) for k, v in out.items()}
+    ref = oracle.score(H, W, hq_o, hs_o, wq_o, ws_o, scaling, ids)
+    _compare(res, ref, V)
