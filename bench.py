@@ -250,10 +250,63 @@ def main():
         "roofline_other": roof_mu if dominant is roof_pi else roof_pi,
     }
 
+    line["config"]["hbm_kernels"] = hbm_kernels(torch, acrl, dev, H, w)
+
     # ---------------- CPU baseline: the oracle on host cores, bounded sample
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, T, H, W, hq, hs, wq, ws, ids, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+
+
+def hbm_kernels(torch, acrl, dev, H, w, reps=5):
+    """Achieved HBM bandwidth of the streaming kernels against 8 TB/s: the
+    three quantizers on this workload's hidden states, and the discrepancy
+    reduce on a dedicated 64M-slot batch (at the workload's 262k slots it is
+    launch-bound)."""
+    T, d = H.shape
+    res = {}
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    for name, scaling, bytes_per_elt in (("quantize_h_per_tensor", inputs.PER_TENSOR, 5.0),
+                                         ("quantize_h_per_row", inputs.PER_ROW, 3.0),
+                                         ("quantize_h_mx32", inputs.MX32, 3.0 + 1.0 / 32)):
+        q, sc = acrl.acrl_quantize_fp8(H, scaling)
+        ms = timed(lambda: acrl.acrl_quantize_fp8(H, scaling, q=q, scales=sc))
+        nbytes = T * d * bytes_per_elt
+        res[name] = {"ms": round(ms, 4), "GBps": round(nbytes / ms / 1e6, 1),
+                     "frac_of_8TBps": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4),
+                     "bytes": int(nbytes)}
+        del q, sc
+    # reduce: 16384 sequences x 4096 slots, lengths U[1, 4096], 17 bytes per slot
+    B, L, ng = 16384, 4096, 2048
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    lp_pi = -torch.rand(B * L, device=dev, generator=g) * 10
+    lp_mu = lp_pi + 0.05 * torch.randn(B * L, device=dev, generator=g)
+    ent = torch.rand(B * L, device=dev, generator=g) * 9
+    lens = torch.randint(1, L + 1, (B,), device=dev, generator=g)
+    mask = (torch.arange(L, device=dev)[None, :] < lens[:, None]).to(torch.uint8).reshape(-1)
+    groups = (torch.arange(B, device=dev, dtype=torch.int32) // 8).contiguous()
+    ms = timed(lambda: acrl.acrl_discrepancy_reduce(B, L, ng, lp_pi, lp_mu, mask, groups, entropy_pi=ent,
+                                                    entropy_mu=ent, want_d_tok=False))
+    nbytes = B * L * 17.0
+    res["reduce_64M_slots"] = {"ms": round(ms, 4), "GBps": round(nbytes / ms / 1e6, 1),
+                               "frac_of_8TBps": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4),
+                               "bytes": int(nbytes)}
+    del lp_pi, lp_mu, ent, mask
+    torch.cuda.empty_cache()
+    log("HBM kernels:", res)
+    return res
 
 
 def cpu_baseline(w, T, H, W, hq, hs, wq, ws, ids, budget_s):
