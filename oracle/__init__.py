@@ -98,6 +98,10 @@ def lib() -> ctypes.CDLL:
         L.acrl_ref_reference_x.argtypes = [P, P, I64, P]
         L.acrl_ref_sample_inverse_cdf.restype = I32
         L.acrl_ref_sample_inverse_cdf.argtypes = [P, I64, I64, P, P]
+        L.acrl_ref_surrogate.restype = I32
+        L.acrl_ref_surrogate.argtypes = [I64, I64, P, P, I64, P, P, P, I32, P, D, D, P, P]
+        L.acrl_ref_lm_head_backward.restype = I32
+        L.acrl_ref_lm_head_backward.argtypes = [I64, I64, I64, P, P, P, P, D, I64, P, P, P, I64, P, P, P]
         _lib = L
     return _lib
 
@@ -294,3 +298,48 @@ def gumbel_sample(z: np.ndarray, seed: int, row_offset: int = 0):
     _check(lib().acrl_ref_gumbel_sample(_p(z), n_rows, V, seed, row_offset, _p(ids), _p(keys)),
            "gumbel_sample")
     return ids, keys
+
+
+# ------------------------------------------------- surrogate and backward
+def surrogate(B: int, L: int, mask, group_of_seq, n_groups: int, logp_new, logp_old, adv,
+              adv_per_token: bool = False, weight=None, eps_low: float = 0.2,
+              eps_high: float = 0.2):
+    """(coef [B*L], loss): d loss/d logp_new and loss = -J of Eq. ACRL."""
+    m = _c(mask, np.uint8).ravel()
+    g = _c(group_of_seq, np.int32)
+    ln = _c(logp_new, np.float64).ravel()
+    lo = _c(logp_old, np.float64).ravel()
+    a = _c(adv, np.float64).ravel()
+    wt = None if weight is None else _c(weight, np.float64).ravel()
+    coef = np.empty(B * L, np.float64)
+    loss = np.empty(1, np.float64)
+    _check(lib().acrl_ref_surrogate(B, L, _p(m), _p(g), n_groups, _p(ln), _p(lo), _p(a),
+                                    int(adv_per_token), _p(wt), eps_low, eps_high, _p(coef),
+                                    _p(loss)), "surrogate")
+    return coef, float(loss[0])
+
+
+def lm_head_backward(h, w, ids, coef, inv_temperature: float = 1.0, hrows=None, wrows=None,
+                     want_abs: bool = False):
+    """Rows of dH = dZ W and dW = dZ^T H (float64), dZ = coef (onehot - p) / tau.
+
+    h: bf16 bits [n, d]; w: bf16 bits [V, d]; hrows / wrows: the rows wanted
+    (None = all).  Returns (dh, dw) or, with want_abs, (dh, dw, dh_abs, dw_abs).
+    """
+    h = _c(h, np.uint16)
+    w = _c(w, np.uint16)
+    n, d = h.shape
+    V = w.shape[0]
+    ids = _c(ids, np.int32)
+    cf = _c(coef, np.float64)
+    hr = np.arange(n, dtype=np.int64) if hrows is None else _c(hrows, np.int64)
+    wr = np.arange(V, dtype=np.int64) if wrows is None else _c(wrows, np.int64)
+    dh = np.empty((hr.size, d), np.float64)
+    dw = np.empty((wr.size, d), np.float64)
+    dha = np.empty((hr.size, d), np.float64) if want_abs else None
+    dwa = np.empty((wr.size, d), np.float64) if want_abs else None
+    _check(lib().acrl_ref_lm_head_backward(n, d, V, _p(h), _p(w), _p(ids), _p(cf), inv_temperature,
+                                           hr.size, _p(hr), _p(dh), _p(dha), wr.size, _p(wr), _p(dw),
+                                           _p(dwa)), "lm_head_backward")
+    return (dh, dw, dha, dwa) if want_abs else (dh, dw)
+

@@ -607,3 +607,130 @@ int acrl_ref_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t 
   }
   return 0;
 }
+
+/* ------------------------------------------------------------------ */
+/* The ACRL-weighted surrogate (Eq. ACRL) and its LM-head backward      */
+/* ------------------------------------------------------------------ */
+
+int acrl_ref_surrogate(int64_t B, int64_t L, const uint8_t* mask, const int32_t* group_of_seq,
+                       int64_t n_groups, const double* logp_new, const double* logp_old,
+                       const double* adv, int adv_per_token, const double* weight,
+                       double eps_low, double eps_high, double* coef, double* loss) {
+  if (B < 0 || L < 0 || n_groups < 0 || !mask || !group_of_seq || !logp_new || !logp_old ||
+      !adv || !coef || !loss)
+    return -1;
+  if (!(eps_low >= 0.0) || !(eps_high >= 0.0)) return -1;
+  for (int64_t i = 0; i < B; ++i)
+    if (group_of_seq[i] < 0 || group_of_seq[i] >= n_groups) return -1;
+  /* |a_i|, then the non-empty responses of each prompt, then the prompts */
+  int64_t* n = (int64_t*)calloc((size_t)(B > 0 ? B : 1), sizeof(int64_t));
+  int64_t* G = (int64_t*)calloc((size_t)(n_groups > 0 ? n_groups : 1), sizeof(int64_t));
+  if (!n || !G) {
+    free(n);
+    free(G);
+    return -1;
+  }
+  for (int64_t i = 0; i < B; ++i)
+    for (int64_t j = 0; j < L; ++j) n[i] += mask[i * L + j] != 0;
+  for (int64_t i = 0; i < B; ++i)
+    if (n[i] > 0) G[group_of_seq[i]] += 1;
+  int64_t prompts = 0;
+  for (int64_t g = 0; g < n_groups; ++g) prompts += G[g] > 0;
+  double J = 0.0;
+  for (int64_t i = 0; i < B; ++i) {
+    for (int64_t j = 0; j < L; ++j) {
+      const int64_t t = i * L + j;
+      coef[t] = 0.0;
+      if (!mask[t]) continue;
+      const double c = 1.0 / ((double)prompts * (double)G[group_of_seq[i]] * (double)n[i]);
+      const double A = adv_per_token ? adv[t] : adv[i];
+      const double wt = weight ? weight[t] : 1.0;
+      const double r = exp(logp_new[t] - logp_old[t]);
+      double rc = r;
+      if (rc < 1.0 - eps_low) rc = 1.0 - eps_low;
+      if (rc > 1.0 + eps_high) rc = 1.0 + eps_high;
+      const double unclipped = r * A, clipped = rc * A;
+      const double m = unclipped <= clipped ? unclipped : clipped;
+      J += c * wt * m;
+      /* d(r A)/d logp_new = r A; the clipped term is constant in logp_new */
+      if (unclipped <= clipped) coef[t] = -c * wt * r * A;
+    }
+  }
+  *loss = -J;
+  free(n);
+  free(G);
+  return 0;
+}
+
+int acrl_ref_lm_head_backward(int64_t n_rows, int64_t d, int64_t V, const uint16_t* h,
+                              const uint16_t* w, const int32_t* ids, const double* coef,
+                              double inv_temperature, int64_t n_hrows, const int64_t* hrows,
+                              double* dh, double* dh_abs, int64_t n_wrows, const int64_t* wrows,
+                              double* dw, double* dw_abs) {
+  if (n_rows < 0 || d <= 0 || V <= 0 || !h || !w || !ids || !coef) return -1;
+  if ((n_hrows > 0 && (!hrows || !dh)) || (n_wrows > 0 && (!wrows || !dw))) return -1;
+  for (int64_t t = 0; t < n_rows; ++t)
+    if (ids[t] < 0 || ids[t] >= V) return -1;
+  for (int64_t i = 0; i < n_hrows; ++i)
+    if (hrows[i] < 0 || hrows[i] >= n_rows) return -1;
+  for (int64_t j = 0; j < n_wrows; ++j)
+    if (wrows[j] < 0 || wrows[j] >= V) return -1;
+  /* dZ of every token, one row at a time: the logits, their log-sum-exp,
+   * then coef (delta - p) / tau */
+  double* dz = (double*)malloc((size_t)(n_rows > 0 ? n_rows : 1) * (size_t)V * sizeof(double));
+  if (!dz) return -1;
+  int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1) reduction(| : bad)
+  for (int64_t t = 0; t < n_rows; ++t) {
+    double* z = dz + t * V;
+    if (acrl_ref_logits_pi(h + t * d, w, d, V, inv_temperature, z)) {
+      bad = 1;
+      continue;
+    }
+    double lse;
+    acrl_ref_token_stats(z, V, ids[t], &lse, NULL, NULL);
+    for (int64_t v = 0; v < V; ++v) {
+      const double p = exp(z[v] - lse);
+      z[v] = coef[t] * ((v == ids[t] ? 1.0 : 0.0) - p) * inv_temperature;
+    }
+  }
+  if (bad) {
+    free(dz);
+    return -1;
+  }
+  /* dH[t, k] = sum_v dZ[t, v] W[v, k]  (v ascending; the row of W is the
+   * inner loop only so that memory is walked in order) */
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t i = 0; i < n_hrows; ++i) {
+    const double* zr = dz + hrows[i] * V;
+    double* s = dh + i * d;
+    for (int64_t k = 0; k < d; ++k) {
+      s[k] = 0.0;
+      if (dh_abs) dh_abs[i * d + k] = 0.0;
+    }
+    for (int64_t v = 0; v < V; ++v)
+      for (int64_t k = 0; k < d; ++k) {
+        const double wv = acrl_ref_bf16_to_float(w[v * d + k]);
+        s[k] += zr[v] * wv;
+        if (dh_abs) dh_abs[i * d + k] += fabs(zr[v]) * fabs(wv);
+      }
+  }
+  /* dW[v, k] = sum_t dZ[t, v] H[t, k]  (t ascending) */
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t j = 0; j < n_wrows; ++j) {
+    const int64_t v = wrows[j];
+    double* s = dw + j * d;
+    for (int64_t k = 0; k < d; ++k) {
+      s[k] = 0.0;
+      if (dw_abs) dw_abs[j * d + k] = 0.0;
+    }
+    for (int64_t t = 0; t < n_rows; ++t)
+      for (int64_t k = 0; k < d; ++k) {
+        const double hv = acrl_ref_bf16_to_float(h[t * d + k]);
+        s[k] += dz[t * V + v] * hv;
+        if (dw_abs) dw_abs[j * d + k] += fabs(dz[t * V + v]) * fabs(hv);
+      }
+  }
+  free(dz);
+  return 0;
+}

@@ -160,6 +160,39 @@ int acrl_ref_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t 
 int acrl_ref_sample_inverse_cdf(const double* z, int64_t n_rows, int64_t V,
                                 const double* u, int32_t* ids);
 
+/* ---- The ACRL-weighted surrogate and its LM-head backward ------------- *
+ * Eq. ACRL (Sec. 4.1), which extends Eq. grpo_objective (Sec. 2.1): the
+ * objective of a batch is
+ *   J = mean over prompts of (1/G) sum_i (1/|a_i|) sum_t w_t min(r_t A_t, clip(r_t) A_t),
+ * r_t = pi_theta(a_t) / pi_theta_old(a_t) = exp(logp_new - logp_old),
+ * clip(r) = min(max(r, 1 - eps_low), 1 + eps_high) (eps_low = eps_high = eps
+ * in the paper), w_t = min(rho_t, C) the controller weight (held constant).
+ * Readings: the prompts averaged are the groups with a non-empty response,
+ * G is the count of the group's non-empty responses (as for Y), an empty
+ * response contributes nothing; loss = -J.
+ * coef[t] = d loss / d logp_new[t] = -c_t w_t r_t A_t when the unclipped term
+ * is the minimum (r A <= clip(r) A; a tie counts as unclipped), else 0;
+ * c_t = 1 / (n_prompts * G_g * |a_i|).  Masked slots: coef 0.
+ * weight NULL means w = 1 (plain GRPO).                                    */
+int acrl_ref_surrogate(int64_t B, int64_t L, const uint8_t* mask, const int32_t* group_of_seq,
+                       int64_t n_groups, const double* logp_new, const double* logp_old,
+                       const double* adv, int adv_per_token, const double* weight,
+                       double eps_low, double eps_high, double* coef, double* loss);
+
+/* Gradient of Phi(H, W) = sum_t coef_t log softmax(W h_t / tau)[a_t] with
+ * respect to H [n_rows, d] and W [V, d] (bf16 bit patterns), by the chain
+ * rule through the surrogate: dZ[t, v] = coef_t (delta(v, a_t) - p_tv) / tau,
+ * p_t = softmax(W h_t / tau); dH = dZ W, dW = dZ^T H, all in double.
+ * Only the requested rows are formed: dh[i, :] = dH[hrows[i], :],
+ * dw[j, :] = dW[wrows[j], :].  dh_abs / dw_abs (nullable) receive
+ * sum_v |dZ[t, v]| |W[v, k]| and sum_t |dZ[t, v]| |H[t, k]|, the magnitude a
+ * rounding error of each product is relative to.  ids must lie in [0, V).   */
+int acrl_ref_lm_head_backward(int64_t n_rows, int64_t d, int64_t V, const uint16_t* h,
+                              const uint16_t* w, const int32_t* ids, const double* coef,
+                              double inv_temperature, int64_t n_hrows, const int64_t* hrows,
+                              double* dh, double* dh_abs, int64_t n_wrows, const int64_t* wrows,
+                              double* dw, double* dw_abs);
+
 #ifdef __cplusplus
 }
 #endif
