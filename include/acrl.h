@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ACRL_ABI_VERSION 2
+#define ACRL_ABI_VERSION 3
 
 typedef int acrl_status;
 enum {
@@ -93,10 +93,10 @@ enum {
 const char* acrl_status_string(acrl_status status);
 const char* acrl_last_error(void);
 int acrl_abi_version(void);
-/* sizeof of the four descriptor structs as compiled into the library (host);
- * bindings compare them with their own layout.                              */
+/* sizeof of the descriptor structs as compiled into the library (host);
+ * bindings compare them with their own layout.  Any pointer may be NULL.    */
 void acrl_abi_struct_sizes(size_t* score_desc, size_t* reduce_desc, size_t* controller_desc,
-                           size_t* sample_desc);
+                           size_t* sample_desc, size_t* surrogate_desc, size_t* backward_desc);
 
 /* ======================================================================== */
 /* a1/a2  acrl_quantize_fp8 -- FP8 quantization of a bf16 matrix            */
@@ -310,6 +310,94 @@ typedef struct acrl_controller_desc {
 } acrl_controller_desc;
 
 acrl_status acrl_controller_step(const acrl_controller_desc* desc, void* stream);
+
+/* ======================================================================== */
+/* acrl_surrogate -- the ACRL-weighted clipped surrogate and d loss/d logp   */
+/* ======================================================================== *
+ * Eq. ACRL (Sec. 4.1) weights the clipped objective of Eq. grpo_objective
+ * (Sec. 2.1) token by token with w_t = min(rho_t, C):
+ *   J = (1/P) sum_g (1/G_g) sum_{i in g} (1/|a_i|) sum_t w_t min(r_t A_t, clip(r_t) A_t),
+ *   r_t = exp(logp_new - logp_old), clip(r) = min(max(r, 1 - eps_low), 1 + eps_high),
+ * over the valid slots (mask != 0); G_g counts the non-empty responses of
+ * prompt g and P the prompts with at least one (empty responses contribute
+ * nothing).  loss[0] = -J (fp64).  coef[t] = d loss / d logp_new[t] =
+ * -w_t r_t A_t / (P G_g |a_i|) where the unclipped term is the minimum (a tie
+ * counts as unclipped), 0 where the clipped term is, 0 for masked slots,
+ * NaN for a response whose group id lies outside [0, n_groups).  w_t is held
+ * constant (it is the controller's output for the behaviour policy);
+ * weight == NULL means w = 1 (plain GRPO).  r, the clip and the sums are
+ * evaluated in fp64 from the fp32 inputs.
+ * Requirements: B, L, n_groups >= 0 (n_groups > 0 if B > 0);
+ * eps_low in [0, 1), eps_high >= 0; workspace of
+ * acrl_surrogate_workspace_size() bytes.                                    */
+typedef struct acrl_surrogate_desc {
+  int64_t B;
+  int64_t L;
+  int64_t n_groups;
+  const uint8_t* mask;          /* [B*L]                                                    */
+  const int32_t* group_of_seq;  /* [B]                                                      */
+  const float* logp_new;        /* [B*L] log pi_theta(a_t) of the policy being trained       */
+  const float* logp_old;        /* [B*L] log pi_theta_old(a_t)                              */
+  const float* adv;             /* [B] or [B*L] advantages A                                */
+  int32_t adv_per_token;        /* 0: adv is [B]; 1: adv is [B*L]                           */
+  float eps_low;                /* clip range of r: [1 - eps_low, 1 + eps_high]             */
+  float eps_high;
+  const float* weight;          /* [B*L] w_t = min(rho, C) (acrl_controller_step), nullable */
+  float* coef;                  /* [B*L] out: d loss / d logp_new                           */
+  double* loss;                 /* [1] out: -J                                              */
+  void* workspace;
+  size_t workspace_bytes;
+} acrl_surrogate_desc;
+
+acrl_status acrl_surrogate_workspace_size(int64_t B, int64_t n_groups, size_t* bytes);
+acrl_status acrl_surrogate(const acrl_surrogate_desc* desc, void* stream);
+
+/* ======================================================================== */
+/* acrl_lm_head_backward -- gradient of the surrogate w.r.t. H and W        */
+/* ======================================================================== *
+ * With z_t = (W h_t) / tau (bf16 operands, fp32 accumulation) and
+ * p_t = softmax(z_t), the loss depends on H and W through
+ * logp_new[t] = z_t[a_t] - lse_t, so by the chain rule
+ *   dZ[t, v] = coef_t (delta(v, a_t) - p_tv) / tau,
+ *   dH = dZ W  ([n_rows, d]),   dW = dZ^T H  ([V, d]).
+ * p is recomputed from the logits and the row's lse (acrl_score_pi_mu's
+ * lse_pi output for the same h, W, tau); dZ is rounded to bf16 and lives only
+ * in the workspace (one pass of token_chunk rows at a time); dH and dW are
+ * the products of the bf16 operands accumulated in fp32.  Rows with coef 0
+ * (masked slots) contribute nothing.  An id outside [0, V) contributes no
+ * one-hot term.
+ *   coef, lse  slot arrays: row r reads slot row_slot[r] (r if row_slot is NULL).
+ *   dh         [n_rows, d] fp32 out, nullable (not computed).
+ *   dw         [V, d] fp32 out, nullable; dw = dW, or dw += dW with
+ *              accumulate_dw = 1 (chunked calls).
+ * Requirements: n_rows >= 0; d > 0, d % 128 == 0; 0 < V < 2^23;
+ * (V rounded up to 256) * d / 8 < 2^32; token_chunk >= 0 (0 = 16384; rounded
+ * up to a multiple of 256; at most 2^23); workspace of
+ * acrl_backward_workspace_size() bytes (packed W, W^T, one chunk of H, H^T
+ * and two bf16 copies of its dZ: about 4 V d + 4 c d + 4 c V bytes for a
+ * chunk of c rows).                                                         */
+typedef struct acrl_backward_desc {
+  int64_t n_rows;
+  int64_t d;
+  int64_t V;
+  const void* h;                /* bf16 [n_rows, d]                                         */
+  const void* w;                /* bf16 [V, d]                                              */
+  const int32_t* token_ids;     /* [n_rows] a_t                                             */
+  const int32_t* row_slot;      /* [n_rows] slot of each row in coef / lse; NULL = identity */
+  const float* coef;            /* [slots] d loss / d logp_new (acrl_surrogate)             */
+  const float* lse;             /* [slots] log-sum-exp of pi's logits (natural units)       */
+  float inv_temperature;        /* 1/tau (> 0), as in the forward pass                      */
+  float* dh;                    /* [n_rows, d] out, nullable                                */
+  float* dw;                    /* [V, d] out, nullable                                     */
+  int32_t accumulate_dw;        /* 1: dw += dW                                              */
+  int64_t token_chunk;          /* rows per internal pass (0 = default)                     */
+  void* workspace;
+  size_t workspace_bytes;
+} acrl_backward_desc;
+
+acrl_status acrl_backward_workspace_size(int64_t n_rows, int64_t d, int64_t V, int64_t token_chunk,
+                                         size_t* bytes);
+acrl_status acrl_lm_head_backward(const acrl_backward_desc* desc, void* stream);
 
 /* Host helper (host pointers): the reference discrepancy X of Sec. 4.1 is the
  * mean of Y_g over the non-empty groups (group_nseq > 0) of the step-0

@@ -32,6 +32,8 @@ EXPORTED = [
     "acrl_score_workspace_size", "acrl_score_pi_mu", "acrl_trace_score_events",
     "acrl_reduce_workspace_size", "acrl_discrepancy_reduce",
     "acrl_controller_step", "acrl_reference_from_groups", "acrl_sample_mu",
+    "acrl_surrogate_workspace_size", "acrl_surrogate",
+    "acrl_backward_workspace_size", "acrl_lm_head_backward",
 ]
 
 _P = ctypes.c_void_p
@@ -70,6 +72,20 @@ class ControllerDesc(ctypes.Structure):
                 ("seq_sum_logratio", _P)]
 
 
+class SurrogateDesc(ctypes.Structure):
+    _fields_ = [("B", _I64), ("L", _I64), ("n_groups", _I64),
+                ("mask", _P), ("group_of_seq", _P), ("logp_new", _P), ("logp_old", _P),
+                ("adv", _P), ("adv_per_token", _I32), ("eps_low", _F32), ("eps_high", _F32),
+                ("weight", _P), ("coef", _P), ("loss", _P), ("workspace", _P), ("workspace_bytes", _SZ)]
+
+
+class BackwardDesc(ctypes.Structure):
+    _fields_ = [("n_rows", _I64), ("d", _I64), ("V", _I64), ("h", _P), ("w", _P),
+                ("token_ids", _P), ("row_slot", _P), ("coef", _P), ("lse", _P),
+                ("inv_temperature", _F32), ("dh", _P), ("dw", _P), ("accumulate_dw", _I32),
+                ("token_chunk", _I64), ("workspace", _P), ("workspace_bytes", _SZ)]
+
+
 class SampleDesc(ctypes.Structure):
     _fields_ = [("n_rows", _I64), ("d", _I64), ("V", _I64),
                 ("hq", _P), ("hq_scales", _P), ("wq", _P), ("wq_scales", _P),
@@ -104,7 +120,7 @@ def lib() -> ctypes.CDLL:
         L.acrl_last_error.argtypes = []
         L.acrl_abi_version.restype = _I32
         L.acrl_abi_struct_sizes.restype = None
-        L.acrl_abi_struct_sizes.argtypes = [ctypes.POINTER(_SZ)] * 4
+        L.acrl_abi_struct_sizes.argtypes = [ctypes.POINTER(_SZ)] * 6
         L.acrl_quantize_workspace_size.restype = _I32
         L.acrl_quantize_workspace_size.argtypes = [_I64, _I64, _I32, ctypes.POINTER(_SZ)]
         L.acrl_quantize_fp8.restype = _I32
@@ -127,10 +143,18 @@ def lib() -> ctypes.CDLL:
         L.acrl_reference_from_groups.argtypes = [_P, _P, _I64, ctypes.POINTER(_F32)]
         L.acrl_sample_mu.restype = _I32
         L.acrl_sample_mu.argtypes = [ctypes.POINTER(SampleDesc), _P]
-        sizes = [_SZ(), _SZ(), _SZ(), _SZ()]
+        L.acrl_surrogate_workspace_size.restype = _I32
+        L.acrl_surrogate_workspace_size.argtypes = [_I64, _I64, ctypes.POINTER(_SZ)]
+        L.acrl_surrogate.restype = _I32
+        L.acrl_surrogate.argtypes = [ctypes.POINTER(SurrogateDesc), _P]
+        L.acrl_backward_workspace_size.restype = _I32
+        L.acrl_backward_workspace_size.argtypes = [_I64, _I64, _I64, _I64, ctypes.POINTER(_SZ)]
+        L.acrl_lm_head_backward.restype = _I32
+        L.acrl_lm_head_backward.argtypes = [ctypes.POINTER(BackwardDesc), _P]
+        sizes = [_SZ() for _ in range(6)]
         L.acrl_abi_struct_sizes(*[ctypes.byref(s) for s in sizes])
         want = [ctypes.sizeof(ScoreDesc), ctypes.sizeof(ReduceDesc), ctypes.sizeof(ControllerDesc),
-                ctypes.sizeof(SampleDesc)]
+                ctypes.sizeof(SampleDesc), ctypes.sizeof(SurrogateDesc), ctypes.sizeof(BackwardDesc)]
         got = [s.value for s in sizes]
         if got != want:
             raise RuntimeError("libacrl descriptor layout mismatch: library %s, binding %s" % (got, want))
@@ -348,3 +372,55 @@ def acrl_reference_from_groups(group_y, group_nseq) -> float:
     _check(lib().acrl_reference_from_groups(gy.ctypes.data_as(_P), gn.ctypes.data_as(_P), gy.size,
                                             ctypes.byref(X)), "acrl_reference_from_groups")
     return float(X.value)
+
+
+# ------------------------------------------------------------------ surrogate and its backward
+def acrl_surrogate(B: int, L: int, n_groups: int, mask, group_of_seq, logp_new, logp_old, adv,
+                   adv_per_token: bool, eps_low: float = 0.2, eps_high: float = 0.2, weight=None,
+                   coef=None, stream=None):
+    """ACRL-weighted clipped surrogate: returns (coef float32 [B*L], loss float64 [1])."""
+    dev = logp_new.device
+    if coef is None:
+        coef = torch.empty(B * L, dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float64, device=dev)
+    nb = _SZ()
+    _check(lib().acrl_surrogate_workspace_size(B, n_groups, ctypes.byref(nb)), "acrl_surrogate_workspace_size")
+    ws = torch.empty(max(nb.value, 256), dtype=torch.uint8, device=dev)
+    desc = SurrogateDesc(B=B, L=L, n_groups=n_groups, mask=_ptr(mask), group_of_seq=_ptr(group_of_seq),
+                         logp_new=_ptr(logp_new), logp_old=_ptr(logp_old), adv=_ptr(adv),
+                         adv_per_token=int(bool(adv_per_token)), eps_low=float(eps_low),
+                         eps_high=float(eps_high), weight=_ptr(weight), coef=_ptr(coef), loss=_ptr(loss),
+                         workspace=_ptr(ws), workspace_bytes=ws.numel())
+    _check(lib().acrl_surrogate(ctypes.byref(desc), _stream(stream)), "acrl_surrogate")
+    coef._acrl_ws = ws  # keep the workspace alive until the stream has consumed it
+    return coef, loss
+
+
+def acrl_lm_head_backward(h, w, token_ids, coef, lse, inv_temperature: float = 1.0, row_slot=None,
+                          want_dh: bool = True, want_dw: bool = True, dh=None, dw=None,
+                          accumulate_dw: bool = False, token_chunk: int = 0, stream=None):
+    """Gradient of the surrogate w.r.t. h [n_rows, d] and w [V, d] (bf16):
+    returns (dh float32 [n_rows, d] or None, dw float32 [V, d] or None)."""
+    _dev(h, torch.bfloat16, "h")
+    _dev(w, torch.bfloat16, "w")
+    _dev(token_ids, torch.int32, "token_ids")
+    _dev(coef, torch.float32, "coef")
+    _dev(lse, torch.float32, "lse")
+    n_rows, d = h.shape
+    V = w.shape[0]
+    dev = h.device
+    if want_dh and dh is None:
+        dh = torch.empty((n_rows, d), dtype=torch.float32, device=dev)
+    if want_dw and dw is None:
+        dw = torch.empty((V, d), dtype=torch.float32, device=dev)
+    nb = _SZ()
+    _check(lib().acrl_backward_workspace_size(n_rows, d, V, int(token_chunk), ctypes.byref(nb)),
+           "acrl_backward_workspace_size")
+    ws = _workspace(nb.value, dev)
+    desc = BackwardDesc(n_rows=n_rows, d=d, V=V, h=_ptr(h), w=_ptr(w), token_ids=_ptr(token_ids),
+                        row_slot=_ptr(row_slot), coef=_ptr(coef), lse=_ptr(lse),
+                        inv_temperature=float(inv_temperature), dh=_ptr(dh if want_dh else None),
+                        dw=_ptr(dw if want_dw else None), accumulate_dw=int(bool(accumulate_dw)),
+                        token_chunk=int(token_chunk), workspace=_ptr(ws), workspace_bytes=nb.value)
+    _check(lib().acrl_lm_head_backward(ctypes.byref(desc), _stream(stream)), "acrl_lm_head_backward")
+    return (dh if want_dh else None), (dw if want_dw else None)

@@ -42,6 +42,23 @@ void set_score_trace(void* const* events, int n);
 hipError_t launch_score(const acrl_score_desc& desc, const ScorePlan& plan, hipStream_t s);
 hipError_t launch_sample(const acrl_sample_desc& desc, const ScorePlan& plan, hipStream_t s);
 
+// LM-head backward of the surrogate: rows are processed in passes of `chunk`
+// tokens; the workspace holds the packed operand images of one pass.
+constexpr int64_t kBackwardChunk = 16384;
+struct BackwardPlan {
+  int64_t chunk;        // rows per pass (a multiple of 256)
+  int n_vtiles;         // vocabulary tiles of 256 rows
+  int n_dtiles;         // hidden-dimension tiles of 256 rows
+  int kch_v;            // 64-byte K chunks of a row whose K runs over the (padded) vocabulary
+  size_t off_w, off_wt, off_h, off_ht, off_zt, off_zv;  // image offsets in the workspace
+  size_t ws_bytes;
+};
+BackwardPlan plan_backward(int64_t n_rows, int64_t d, int64_t V, int64_t chunk);
+hipError_t launch_backward(const acrl_backward_desc& desc, const BackwardPlan& plan, hipStream_t s);
+
+size_t surrogate_workspace_bytes(int64_t B, int64_t n_groups);
+hipError_t launch_surrogate(const acrl_surrogate_desc& desc, hipStream_t s);
+
 size_t reduce_workspace_bytes(int64_t B, int64_t L, int64_t n_groups);
 hipError_t launch_reduce(const acrl_reduce_desc& desc, hipStream_t s);
 hipError_t launch_controller(const acrl_controller_desc& desc, hipStream_t s);

@@ -143,11 +143,13 @@ const char* acrl_last_error(void) { return acrl::g_last_error; }
 int acrl_abi_version(void) { return ACRL_ABI_VERSION; }
 
 void acrl_abi_struct_sizes(size_t* score_desc, size_t* reduce_desc, size_t* controller_desc,
-                           size_t* sample_desc) {
+                           size_t* sample_desc, size_t* surrogate_desc, size_t* backward_desc) {
   if (score_desc) *score_desc = sizeof(acrl_score_desc);
   if (reduce_desc) *reduce_desc = sizeof(acrl_reduce_desc);
   if (controller_desc) *controller_desc = sizeof(acrl_controller_desc);
   if (sample_desc) *sample_desc = sizeof(acrl_sample_desc);
+  if (surrogate_desc) *surrogate_desc = sizeof(acrl_surrogate_desc);
+  if (backward_desc) *backward_desc = sizeof(acrl_backward_desc);
 }
 
 acrl_status acrl_quantize_workspace_size(int64_t rows, int64_t cols, int scaling, size_t* bytes) {
@@ -317,6 +319,83 @@ acrl_status acrl_controller_step(const acrl_controller_desc* d, void* stream) {
   acrl_status st = acrl::check_device();
   if (st != ACRL_OK) return st;
   return acrl::hip_status(acrl::launch_controller(*d, (hipStream_t)stream), "acrl_controller_step launch");
+}
+
+acrl_status acrl_surrogate_workspace_size(int64_t B, int64_t n_groups, size_t* bytes) {
+  ACRL_REQUIRE(bytes, "bytes is NULL");
+  ACRL_REQUIRE(B >= 0 && n_groups >= 0, "B and n_groups must be >= 0");
+  *bytes = acrl::surrogate_workspace_bytes(B, n_groups);
+  return ACRL_OK;
+}
+
+acrl_status acrl_surrogate(const acrl_surrogate_desc* d, void* stream) {
+  ACRL_REQUIRE(d, "desc is NULL");
+  ACRL_REQUIRE(d->B >= 0 && d->L >= 0 && d->n_groups >= 0, "B, L and n_groups must be >= 0");
+  ACRL_REQUIRE(d->B < (int64_t)INT32_MAX && d->n_groups < (int64_t)INT32_MAX, "B or n_groups too large");
+  ACRL_REQUIRE(d->B == 0 || d->n_groups > 0, "n_groups must be > 0 when B > 0");
+  ACRL_REQUIRE(d->eps_low >= 0.0f && d->eps_low < 1.0f, "eps_low must lie in [0, 1) (got %g)", (double)d->eps_low);
+  ACRL_REQUIRE(d->eps_high >= 0.0f && d->eps_high < 1e30f, "eps_high must be >= 0 (got %g)", (double)d->eps_high);
+  ACRL_REQUIRE(d->loss, "loss is required");
+  if (d->B > 0) ACRL_REQUIRE(d->group_of_seq, "group_of_seq is required");
+  if (d->B > 0 && d->L > 0)
+    ACRL_REQUIRE(d->mask && d->logp_new && d->logp_old && d->adv && d->coef,
+                 "mask, logp_new, logp_old, adv and coef are required");
+  const size_t need = acrl::surrogate_workspace_bytes(d->B, d->n_groups);
+  if (!d->workspace || d->workspace_bytes < need) {
+    set_error("acrl_surrogate needs %zu workspace bytes, got %zu", need, d->workspace_bytes);
+    return ACRL_ERR_WORKSPACE;
+  }
+  acrl_status st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(acrl::launch_surrogate(*d, (hipStream_t)stream), "acrl_surrogate launch");
+}
+
+static acrl_status validate_backward_sizes(int64_t n_rows, int64_t d, int64_t V, int64_t chunk) {
+  ACRL_REQUIRE(n_rows >= 0 && n_rows < (int64_t)INT32_MAX - 512, "n_rows %lld out of range", (long long)n_rows);
+  ACRL_REQUIRE(d > 0 && d % 128 == 0, "d = %lld must be a positive multiple of 128", (long long)d);
+  ACRL_REQUIRE(V > 0 && V < ((int64_t)1 << 23), "V = %lld must lie in (0, 2^23)", (long long)V);
+  ACRL_REQUIRE(acrl::score_size_ok(V, d), "V x d too large (V rounded up to 256, times d/8, must be below 2^32)");
+  ACRL_REQUIRE(chunk >= 0 && chunk <= ((int64_t)1 << 23), "token_chunk must lie in [0, 2^23]");
+  const int64_t c = acrl::plan_backward(n_rows, d, V, chunk).chunk;
+  ACRL_REQUIRE(acrl::score_size_ok(c, d), "token_chunk x d too large");
+  return ACRL_OK;
+}
+
+acrl_status acrl_backward_workspace_size(int64_t n_rows, int64_t d, int64_t V, int64_t token_chunk, size_t* bytes) {
+  ACRL_REQUIRE(bytes, "bytes is NULL");
+  acrl_status st = validate_backward_sizes(n_rows, d, V, token_chunk);
+  if (st != ACRL_OK) return st;
+  *bytes = acrl::plan_backward(n_rows, d, V, token_chunk).ws_bytes;
+  return ACRL_OK;
+}
+
+acrl_status acrl_lm_head_backward(const acrl_backward_desc* d, void* stream) {
+  ACRL_REQUIRE(d, "desc is NULL");
+  acrl_status st = validate_backward_sizes(d->n_rows, d->d, d->V, d->token_chunk);
+  if (st != ACRL_OK) return st;
+  ACRL_REQUIRE(d->inv_temperature > 0.0f && d->inv_temperature < 1e30f,
+               "inv_temperature must be positive and finite");
+  ACRL_REQUIRE(d->dh || d->dw, "at least one of dh and dw is required");
+  if (d->dw || d->n_rows > 0) {
+    ACRL_REQUIRE(d->w, "w is required");
+    ACRL_REQUIRE(acrl::aligned16(d->w), "w must be 16-byte aligned");
+  }
+  if (d->n_rows > 0) {
+    ACRL_REQUIRE(d->h && d->token_ids && d->coef && d->lse, "h, token_ids, coef and lse are required");
+    ACRL_REQUIRE(acrl::aligned16(d->h), "h must be 16-byte aligned");
+  }
+  const acrl::BackwardPlan plan = acrl::plan_backward(d->n_rows, d->d, d->V, d->token_chunk);
+  if (d->n_rows > 0 && (!d->workspace || d->workspace_bytes < plan.ws_bytes)) {
+    set_error("acrl_lm_head_backward needs %zu workspace bytes, got %zu", plan.ws_bytes, d->workspace_bytes);
+    return ACRL_ERR_WORKSPACE;
+  }
+  if (d->n_rows > 0 && !acrl::aligned16(d->workspace)) {
+    set_error("workspace must be 16-byte aligned");
+    return ACRL_ERR_INVALID_ARG;
+  }
+  st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(acrl::launch_backward(*d, plan, (hipStream_t)stream), "acrl_lm_head_backward launch");
 }
 
 acrl_status acrl_reference_from_groups(const float* group_y, const int32_t* group_nseq, int64_t n_groups,

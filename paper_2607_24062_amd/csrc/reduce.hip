@@ -238,9 +238,145 @@ __global__ __launch_bounds__(256) void controller_kernel(acrl_controller_desc p)
   }
 }
 
+// ------------------------------------------------------------------ surrogate
+// The ACRL-weighted clipped surrogate (Eq. ACRL on top of the GRPO objective
+// of Sec. 2.1): J = mean over prompts of (1/G) sum_i (1/|a_i|) sum_t
+// w_t min(r_t A_t, clip(r_t) A_t), r_t = exp(logp_new - logp_old); the
+// prompts averaged are those with a non-empty response and G counts a
+// prompt's non-empty responses.  loss = -J, coef_t = d loss / d logp_new_t.
+
+struct SurrSeq {
+  double n, J;  // |a_i| and sum_t w_t min(r A, clip(r) A)
+};
+
+// r A, clip(r) A and whether the unclipped term is the minimum (a tie counts
+// as unclipped), in fp64 from the fp32 inputs.
+__device__ __forceinline__ void surr_terms(const acrl_surrogate_desc& p, int64_t t, int64_t i, double& r,
+                                           double& A, double& m, bool& unclipped) {
+  A = p.adv_per_token ? p.adv[t] : p.adv[i];
+  r = exp((double)p.logp_new[t] - (double)p.logp_old[t]);
+  const double rc = fmin(fmax(r, 1.0 - (double)p.eps_low), 1.0 + (double)p.eps_high);
+  const double u = r * A, c = rc * A;
+  unclipped = u <= c;
+  m = unclipped ? u : c;
+}
+
+// One workgroup per response.
+__global__ __launch_bounds__(kRedThreads) void surr_seq_kernel(acrl_surrogate_desc p, SurrSeq* rec) {
+  __shared__ double sh[kRedThreads / 64];
+  const int64_t i = blockIdx.x;
+  double n = 0, J = 0;
+  for (int64_t j = threadIdx.x; j < p.L; j += kRedThreads) {
+    const int64_t t = i * p.L + j;
+    if (!p.mask[t]) continue;
+    double r, A, m;
+    bool unc;
+    surr_terms(p, t, i, r, A, m, unc);
+    n += 1.0;
+    J += (p.weight ? (double)p.weight[t] : 1.0) * m;
+  }
+  n = block_sum(n, sh);
+  J = block_sum(J, sh);
+  if (threadIdx.x == 0) rec[i] = SurrSeq{n, J};
+}
+
+// One workgroup per group: G_g and the group's sum of per-response means.
+__global__ __launch_bounds__(kRedThreads) void surr_group_kernel(acrl_surrogate_desc p, const SurrSeq* rec,
+                                                                 double* gG, double* gJ) {
+  __shared__ double sh[kRedThreads / 64];
+  const int g = blockIdx.x;
+  double G = 0, J = 0;
+  for (int64_t i = threadIdx.x; i < p.B; i += kRedThreads)
+    if (p.group_of_seq[i] == g && rec[i].n > 0) {
+      G += 1.0;
+      J += rec[i].J / rec[i].n;
+    }
+  G = block_sum(G, sh);
+  J = block_sum(J, sh);
+  if (threadIdx.x == 0) {
+    gG[g] = G;
+    gJ[g] = J;
+  }
+}
+
+// One workgroup: the number of prompts and the loss.
+__global__ __launch_bounds__(kRedThreads) void surr_batch_kernel(acrl_surrogate_desc p, const double* gG,
+                                                                 const double* gJ, double* prompts) {
+  __shared__ double sh[kRedThreads / 64];
+  double np = 0, J = 0;
+  for (int64_t g = threadIdx.x; g < p.n_groups; g += kRedThreads)
+    if (gG[g] > 0) {
+      np += 1.0;
+      J += gJ[g] / gG[g];
+    }
+  np = block_sum(np, sh);
+  J = block_sum(J, sh);
+  if (threadIdx.x == 0) {
+    prompts[0] = np;
+    p.loss[0] = np > 0 ? -J / np : 0.0;
+  }
+}
+
+// Element-wise: coef_t = -w_t r_t A_t / (prompts G_g |a_i|) where the
+// unclipped term is the minimum, else 0 (the clipped term does not depend on
+// logp_new); masked slots 0; a group id outside [0, n_groups) gives NaN.
+__global__ __launch_bounds__(256) void surr_coef_kernel(acrl_surrogate_desc p, const SurrSeq* rec, const double* gG,
+                                                        const double* prompts) {
+  const int64_t n = p.B * p.L;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < n; t += (int64_t)gridDim.x * blockDim.x) {
+    float out = 0.0f;
+    if (p.mask[t]) {
+      const int64_t i = t / p.L;
+      const int32_t g = p.group_of_seq[i];
+      if (g < 0 || g >= p.n_groups) {
+        out = __builtin_nanf("");
+      } else {
+        double r, A, m;
+        bool unc;
+        surr_terms(p, t, i, r, A, m, unc);
+        if (unc) {
+          const double c = 1.0 / (prompts[0] * gG[g] * rec[i].n);
+          out = (float)(-c * (p.weight ? (double)p.weight[t] : 1.0) * r * A);
+        }
+      }
+    }
+    p.coef[t] = out;
+  }
+}
+
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 }  // namespace
+
+size_t surrogate_workspace_bytes(int64_t B, int64_t n_groups) {
+  return align_up((size_t)B * sizeof(SurrSeq), 256) + 2 * align_up((size_t)n_groups * sizeof(double), 256) + 256;
+}
+
+hipError_t launch_surrogate(const acrl_surrogate_desc& p, hipStream_t s) {
+  uint8_t* ws = static_cast<uint8_t*>(p.workspace);
+  SurrSeq* rec = reinterpret_cast<SurrSeq*>(ws);
+  size_t off = align_up((size_t)p.B * sizeof(SurrSeq), 256);
+  double* gG = reinterpret_cast<double*>(ws + off);
+  off += align_up((size_t)p.n_groups * sizeof(double), 256);
+  double* gJ = reinterpret_cast<double*>(ws + off);
+  off += align_up((size_t)p.n_groups * sizeof(double), 256);
+  double* prompts = reinterpret_cast<double*>(ws + off);
+  if (p.B > 0)
+    hipLaunchKernelGGL(surr_seq_kernel, dim3((unsigned)p.B), dim3(kRedThreads), 0, s, p, rec);
+  if (p.n_groups > 0)
+    hipLaunchKernelGGL(surr_group_kernel, dim3((unsigned)p.n_groups), dim3(kRedThreads), 0, s, p,
+                       (const SurrSeq*)rec, gG, gJ);
+  hipLaunchKernelGGL(surr_batch_kernel, dim3(1), dim3(kRedThreads), 0, s, p, (const double*)gG, (const double*)gJ,
+                     prompts);
+  const int64_t n = p.B * p.L;
+  if (n > 0) {
+    int64_t g = (n + 255) / 256;
+    if (g > 8192) g = 8192;
+    hipLaunchKernelGGL(surr_coef_kernel, dim3((unsigned)g), dim3(256), 0, s, p, (const SurrSeq*)rec,
+                       (const double*)gG, (const double*)prompts);
+  }
+  return hipGetLastError();
+}
 
 size_t reduce_workspace_bytes(int64_t B, int64_t L, int64_t n_groups) {
   (void)L;

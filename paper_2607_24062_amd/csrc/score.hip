@@ -39,6 +39,14 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 enum ScoreMode { kBF16 = 0, kFP8Tensor = 1, kFP8Row = 2, kMX = 3 };
 
+// What a workgroup does with each finished accumulator tile.
+enum Epilogue {
+  kEpiSoftmax = 0,  // online log-softmax statistics + sampled-token logit (scoring)
+  kEpiSample = 1,   // the same plus a Gumbel-max draw (sampling from mu)
+  kEpiGrad = 2,     // dZ = coef (onehot - softmax) / tau as bf16 operand images (backward)
+  kEpiStore = 3,    // the product tile itself, fp32, stored (optionally on top of C)
+};
+
 constexpr int kTileV = 256;            // vocabulary rows per workgroup tile
 constexpr int kTileT = 256;            // tokens per workgroup tile
 constexpr int kChunk = 64;             // bytes of K per row per pipeline stage
@@ -81,6 +89,20 @@ struct ScoreParams {
   float* best_key;         // [n_strips][n_rows]: the strip's largest Gumbel key (log2 units)
   float* best_logit;       // [n_strips][n_rows]: its logit (natural units)
   int32_t* best_id;        // [n_strips][n_rows]: its vocabulary row
+  // gradient of the surrogate (kEpiGrad) only
+  const float* g_coef;     // [slots] d loss / d logp of each token
+  const float* g_lse;      // [slots] log-sum-exp of pi's logits (natural units)
+  const int32_t* g_slot;   // [n_rows] slot of each row (NULL: slot = row + g_slot_offset)
+  int64_t g_slot_offset;
+  uint8_t* gz_t;           // dZ image, rows = tokens, K = vocabulary: [n_ttiles][kch_v][256][64 B]
+  uint8_t* gz_v;           // dZ image, rows = vocabulary, K = tokens: [n_vtiles][kch_t][256][64 B]
+  int kch_v;               // 64-byte K chunks of a gz_t row (= n_vtiles * 8)
+  int kch_t;               // 64-byte K chunks of a gz_v row (= n_ttiles * 8)
+  // plain product (kEpiStore) only: C[m, n] (m = A row, n = B row), row-major
+  float* c;
+  int64_t ldc;
+  int c_rows;              // valid A rows (M)
+  int c_accumulate;        // 1: C += product (C is read once before the K loop)
 };
 
 // Philox4x32-10 (Salmon et al., SC 2011): 10 rounds on a 128-bit counter
@@ -200,9 +222,12 @@ struct Pipe {
   static constexpr int kLoadsPerChunk = (MODE == kMX) ? 10 : 8;  // per wave, at least
 };
 
-template <int MODE, bool SAMPLE>
+template <int MODE, int EPI>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void score_kernel(ScoreParams p) {
+  constexpr bool SAMPLE = EPI == kEpiSample;
+  constexpr bool SOFTMAX = EPI == kEpiSoftmax || EPI == kEpiSample;
+  static_assert(MODE == kBF16 || SOFTMAX, "the backward epilogues take bf16 operands");
   constexpr int NS = Pipe<MODE>::kStages;
   constexpr int SB = Pipe<MODE>::kScaleBytes;
   constexpr int LPC = Pipe<MODE>::kLoadsPerChunk;
@@ -234,6 +259,7 @@ void score_kernel(ScoreParams p) {
   // ---- per-lane tokens: column r32 of each of the wave's 4 token blocks
   int tok[4], id[4];
   float c2[4], cz[4];
+  float gl2[4], gc[4];  // backward: lse (log2 units) and coef / tau of the lane's tokens
   float M[4], S[4], U[4];
   float bk[4], bz[4];  // sampling: best Gumbel key of the lane and its logit
   int bi[4];           //           and vocabulary row
@@ -241,7 +267,16 @@ void score_kernel(ScoreParams p) {
   for (int j = 0; j < 4; ++j) {
     tok[j] = t0 + wt * 128 + j * 32 + r32;
     const int tc = min(tok[j], p.n_rows - 1);
-    id[j] = SAMPLE ? -1 : p.ids[tc];
+    id[j] = (EPI == kEpiSoftmax || EPI == kEpiGrad) ? p.ids[tc] : -1;
+    gl2[j] = 0.0f;
+    gc[j] = 0.0f;
+    if constexpr (EPI == kEpiGrad) {
+      // rows past the end and rows with coef 0 (masked) get dZ = 0
+      const int64_t slot = p.g_slot ? (int64_t)p.g_slot[tc] : p.g_slot_offset + tc;
+      const float cf = tok[j] < p.n_rows ? p.g_coef[slot] : 0.0f;
+      gc[j] = cf * p.inv_temp;
+      gl2[j] = cf != 0.0f ? p.g_lse[slot] * kLog2e : 0.0f;
+    }
     bk[j] = -INFINITY;
     bz[j] = 0.0f;
     bi[j] = 0;
@@ -260,6 +295,21 @@ void score_kernel(ScoreParams p) {
   for (int b = 0; b < 4; ++b)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
+  if constexpr (EPI == kEpiStore) {
+    // one output tile per workgroup: start from C when accumulating
+    if (p.c_accumulate) {
+      const int m0 = vt_begin * kTileV + wv * 128 + 4 * g;
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int m = m0 + 32 * b + 8 * (i >> 2) + (i & 3);
+            if (m < p.c_rows && tok[j] < p.n_rows) acc[b][j][i] = p.c[(int64_t)m * p.ldc + tok[j]];
+          }
+    }
+  }
 
   // ---- global -> LDS.  A stage holds one 64-byte K chunk of all 256 + 256
   // rows (W tile rows first).  Operands come packed (pack_kernel): the
@@ -523,6 +573,84 @@ void score_kernel(ScoreParams p) {
     else run(std::false_type{});
   };
 
+  // Backward (kEpiGrad): dZ[t, v] = coef_t (delta(v, a_t) - p_tv) / tau of the
+  // finished tile, p = 2^(y - lse2) from the accumulators, rounded to bf16 and
+  // stored into the two operand images of the gradient products: rows =
+  // tokens (K = vocabulary) for dH = dZ W and rows = vocabulary (K = tokens)
+  // for dW = dZ^T H, in the packed layout pack_kernel writes (16-byte column
+  // c of row r at position c ^ ((r/4) % 4) of its 64-byte chunk row).  Rows
+  // past V and tokens past n_rows or with coef 0 store 0 (the select also
+  // drops a non-finite p of such a row).
+  auto grad_epilogue = [&](int tile) {
+    const int vw = tile * kTileV + wv * 128;  // first vocabulary row of this wave
+    const bool odd = (lane & 1) != 0;
+    auto pack2 = [](float lo, float hi) -> uint32_t {
+      return (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) |
+             ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
+    };
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float dz[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int v = vw + 32 * b + 8 * (i >> 2) + 4 * g + (i & 3);
+          const float pr = fast_exp2(fmaf(acc_read(acc[b][j][i]), c2[j], -gl2[j]));
+          const float oh = v == id[j] ? 1.0f : 0.0f;
+          dz[i] = (v < p.V && gc[j] != 0.0f) ? gc[j] * (oh - pr) : 0.0f;
+        }
+        // rows = tokens: the lane's token row, 4 consecutive vocabulary
+        // values (8 bytes) per 16-byte column q
+        {
+          const int rr = wt * 128 + 32 * j + r32;
+          const int kc = tile * 8 + wv * 4 + b;
+          uint8_t* row = p.gz_t + (((int64_t)tt * p.kch_v + kc) * kTileT + rr) * kChunk + 8 * g;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const uint2 w2 = make_uint2(pack2(dz[4 * q], dz[4 * q + 1]), pack2(dz[4 * q + 2], dz[4 * q + 3]));
+            *reinterpret_cast<uint2*>(row + ((q ^ ((rr >> 2) & 3)) << 4)) = w2;
+          }
+        }
+        // rows = vocabulary: lanes 2m, 2m+1 hold tokens 2m, 2m+1 of one row;
+        // after one exchange the even lane stores the pair of row i, the odd
+        // lane the pair of row i+1 (4 bytes each)
+        {
+          const int kc = tt * 8 + wt * 4 + j;
+          uint8_t* img = p.gz_v + ((int64_t)tile * p.kch_t + kc) * kTileV * kChunk;
+#pragma unroll
+          for (int i = 0; i < 16; i += 2) {
+            const float send = odd ? dz[i] : dz[i + 1];
+            const float recv = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(send), 0xB1, 0xF, 0xF, true));
+            const uint32_t w1 = odd ? pack2(recv, dz[i + 1]) : pack2(dz[i], recv);
+            const int row = wv * 128 + 32 * b + 8 * (i >> 2) + 4 * g + (i & 3) + (odd ? 1 : 0);
+            *reinterpret_cast<uint32_t*>(img + row * kChunk + ((((r32 >> 3) ^ ((row >> 2) & 3))) << 4) +
+                                         2 * (r32 & 6)) = w1;
+          }
+        }
+      }
+    }
+    // The pipeline's waits count outstanding vector-memory operations; these
+    // stores would count with the operand loads, so they drain here.
+    wait_vmcnt<0>();
+  };
+
+  // Plain product (kEpiStore): C[m, n] = the tile (after the initial C when
+  // accumulating); m = A row, n = B row; 32 lanes store 32 consecutive n.
+  auto store_epilogue = [&](int tile) {
+    const int m0 = tile * kTileV + wv * 128 + 4 * g;
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int m = m0 + 32 * b + 8 * (i >> 2) + (i & 3);
+          const float x = acc_read(acc[b][j][i]);
+          if (m < p.c_rows && tok[j] < p.n_rows) p.c[(int64_t)m * p.ldc + tok[j]] = x;
+        }
+  };
+
   // ---- the pipeline.  Chunks 0..NS-1 are requested up front, one per
   // stage.  Fragments are read L MFMA groups ahead of their use, so every LDS
   // read is covered by 4L MFMAs.  In chunk c the first read of chunk c+1
@@ -645,12 +773,15 @@ void score_kernel(ScoreParams p) {
       chunk(std::false_type{}, it, f0, f1);
       chunk(std::false_type{}, it + 1, f1, f0);
     }
-    epilogue(vt_begin + q, q);
+    if constexpr (SOFTMAX) epilogue(vt_begin + q, q);
+    else if constexpr (EPI == kEpiGrad) grad_epilogue(vt_begin + q);
+    else store_epilogue(vt_begin + q);
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
       for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
   }
+  if constexpr (!SOFTMAX) return;
   __syncthreads();  // every wave is done with the stages before LDS is reused
 
   // ---- merge the lane pair (l, l^32), then the two vocabulary halves
@@ -732,6 +863,42 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint8_t* __restrict__ s
     const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)sr * row_bytes + piece * 16);
     *reinterpret_cast<uint4*>(dst + ((size_t)(tile * n_chunks + kc) * kTileV + rr) * kChunk + pos * 16) = v;
   }
+}
+
+// Transposed packed image: the rows of the image are the COLUMNS k of
+// x [rows, cols] (bf16) and its K dimension runs along x's rows, in the
+// layout pack_kernel writes (one 16 KiB block per (256-column tile, 32-row
+// chunk); 16-byte column c of image row k at position c ^ ((k/4) % 4)).
+// Rows of x past `rows` and columns past `cols` read as 0.  One workgroup
+// per block: thread t builds image row k = 256 tile + t from 32 loads that
+// the workgroup issues as coalesced 512-byte row segments.
+__global__ __launch_bounds__(256) void pack_t_kernel(const uint16_t* __restrict__ x, int64_t rows, int64_t cols,
+                                                     int n_rchunks, uint8_t* __restrict__ dst) {
+  const int64_t blk = blockIdx.x;
+  const int64_t ktile = blk / n_rchunks, rc = blk % n_rchunks;
+  const int t = threadIdx.x;
+  const int64_t k = ktile * kTileV + t;
+  uint32_t w[16];
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    uint32_t lohi[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int64_t r = rc * 32 + 2 * i + h;
+      lohi[h] = (r < rows && k < cols) ? (uint32_t)x[r * cols + k] : 0u;
+    }
+    w[i] = lohi[0] | (lohi[1] << 16);
+  }
+  uint8_t* row = dst + (blk * kTileV + t) * kChunk;
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    *reinterpret_cast<uint4*>(row + ((c ^ ((t >> 2) & 3)) << 4)) =
+        make_uint4(w[4 * c], w[4 * c + 1], w[4 * c + 2], w[4 * c + 3]);
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, int64_t n) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0.0f;
 }
 
 struct MergeParams {
@@ -928,7 +1095,7 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   pp.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[0]);
   pp.logit = reinterpret_cast<float*>(ws + pl.ws_logit_offset[0]);
   trace(0, s);
-  hipLaunchKernelGGL((score_kernel<kBF16, false>), dim3(grid), dim3(kThreads), 0, s, pp);
+  hipLaunchKernelGGL((score_kernel<kBF16, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pp);
   trace(1, s);
 
   // mu: e4m3 operands
@@ -941,14 +1108,14 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
     pm.a_mx = static_cast<const uint8_t*>(dsc.wq_scales);
     pm.b_mx = static_cast<const uint8_t*>(dsc.hq_scales);
-    hipLaunchKernelGGL((score_kernel<kMX, false>), dim3(grid), dim3(kThreads), 0, s, pm);
+    hipLaunchKernelGGL((score_kernel<kMX, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pm);
   } else {
     pm.a_scale = static_cast<const float*>(dsc.wq_scales);
     pm.b_scale = static_cast<const float*>(dsc.hq_scales);
     if (dsc.mu_scaling == ACRL_SCALE_PER_ROW)
-      hipLaunchKernelGGL((score_kernel<kFP8Row, false>), dim3(grid), dim3(kThreads), 0, s, pm);
+      hipLaunchKernelGGL((score_kernel<kFP8Row, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pm);
     else
-      hipLaunchKernelGGL((score_kernel<kFP8Tensor, false>), dim3(grid), dim3(kThreads), 0, s, pm);
+      hipLaunchKernelGGL((score_kernel<kFP8Tensor, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pm);
   }
 
   trace(2, s);
@@ -970,6 +1137,148 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   mp.error_flag = dsc.error_flag;
   hipLaunchKernelGGL(merge_kernel, dim3((unsigned)((dsc.n_rows + 255) / 256)), dim3(256), 0, s, mp);
   trace(3, s);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ backward
+// Grid of a plain product (kEpiStore): one workgroup per output tile, in the
+// scoring kernel's XCD-aware raster (A tiles play the vocabulary strips, B
+// tiles the token tiles).
+static void gemm_grid(int n_atiles, int n_btiles, ScoreParams& pp, unsigned& grid) {
+  pp.n_vtiles = n_atiles;
+  pp.tiles_per_strip = 1;
+  pp.n_strips = n_atiles;
+  pp.n_ttiles = n_btiles;
+  pp.n_tblocks = (n_btiles + kBlockT - 1) / kBlockT;
+  const int n_sblocks = (n_atiles + kBlockS - 1) / kBlockS;
+  const int blocks = (pp.n_tblocks * n_sblocks + kXcds - 1) / kXcds * kXcds;
+  grid = (unsigned)(blocks * kBlockT * kBlockS);
+}
+
+BackwardPlan plan_backward(int64_t n_rows, int64_t d, int64_t V, int64_t chunk) {
+  BackwardPlan pl{};
+  pl.chunk = chunk <= 0 ? kBackwardChunk : (chunk + kTileT - 1) / kTileT * kTileT;
+  if (n_rows < pl.chunk) pl.chunk = (n_rows + kTileT - 1) / kTileT * kTileT;
+  if (pl.chunk == 0) pl.chunk = kTileT;
+  pl.n_vtiles = (int)((V + kTileV - 1) / kTileV);
+  pl.n_dtiles = (int)((d + kTileV - 1) / kTileV);
+  pl.kch_v = pl.n_vtiles * 8;
+  const int n_ttiles = (int)(pl.chunk / kTileT);
+  const size_t vrows = (size_t)pl.n_vtiles * kTileV, drows = (size_t)pl.n_dtiles * kTileV;
+  const size_t crows = (size_t)pl.chunk;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += align_up(bytes, 256);
+    return o;
+  };
+  pl.off_w = take(vrows * 2 * (size_t)d);                  // W, rows = vocabulary, K = d
+  pl.off_wt = take(drows * vrows * 2);                     // W^T, rows = d, K = vocabulary
+  pl.off_h = take(crows * 2 * (size_t)d);                  // H chunk, rows = tokens, K = d
+  pl.off_ht = take(drows * crows * 2);                     // H^T chunk, rows = d, K = tokens
+  pl.off_zt = take((size_t)n_ttiles * kTileT * vrows * 2); // dZ, rows = tokens, K = vocabulary
+  pl.off_zv = take(vrows * crows * 2);                     // dZ^T, rows = vocabulary, K = tokens
+  pl.ws_bytes = off;
+  return pl;
+}
+
+hipError_t launch_backward(const acrl_backward_desc& dsc, const BackwardPlan& pl, hipStream_t s) {
+  uint8_t* ws = static_cast<uint8_t*>(dsc.workspace);
+  const int64_t d = dsc.d, V = dsc.V;
+  float* dh = dsc.dh;
+  float* dw = dsc.dw;
+  if (dsc.n_rows == 0) {
+    if (dw && !dsc.accumulate_dw)
+      hipLaunchKernelGGL(fill_zero_kernel, dim3(4096), dim3(256), 0, s, dw, V * d);
+    return hipGetLastError();
+  }
+  uint8_t* img_w = ws + pl.off_w;
+  uint8_t* img_wt = ws + pl.off_wt;
+  uint8_t* img_h = ws + pl.off_h;
+  uint8_t* img_ht = ws + pl.off_ht;
+  uint8_t* img_zt = ws + pl.off_zt;
+  uint8_t* img_zv = ws + pl.off_zv;
+  const uint16_t* w = static_cast<const uint16_t*>(dsc.w);
+  const uint16_t* h = static_cast<const uint16_t*>(dsc.h);
+  // W (rows = vocabulary, for the recomputed logits) and W^T (rows = d, for dH), once per call
+  {
+    const int64_t units = (int64_t)pl.n_vtiles * kTileV * (2 * d / 16);
+    hipLaunchKernelGGL(pack_kernel, dim3((unsigned)std::min<int64_t>((units + 255) / 256, 8192)), dim3(256), 0, s,
+                       reinterpret_cast<const uint8_t*>(w), (uint32_t)V, (uint32_t)(2 * d), (uint32_t)units, img_w);
+    if (dh)
+      hipLaunchKernelGGL(pack_t_kernel, dim3((unsigned)((int64_t)pl.n_dtiles * pl.kch_v)), dim3(256), 0, s, w, V, d,
+                         pl.kch_v, img_wt);
+  }
+  for (int64_t r0 = 0; r0 < dsc.n_rows; r0 += pl.chunk) {
+    const int64_t rows = std::min<int64_t>(pl.chunk, dsc.n_rows - r0);
+    const int n_ttiles = (int)((rows + kTileT - 1) / kTileT);
+    const int kch_t = n_ttiles * 8;
+    const int64_t units = (int64_t)n_ttiles * kTileT * (2 * d / 16);
+    hipLaunchKernelGGL(pack_kernel, dim3((unsigned)std::min<int64_t>((units + 255) / 256, 8192)), dim3(256), 0, s,
+                       reinterpret_cast<const uint8_t*>(h + r0 * d), (uint32_t)rows, (uint32_t)(2 * d),
+                       (uint32_t)units, img_h);
+    if (dw)
+      hipLaunchKernelGGL(pack_t_kernel, dim3((unsigned)((int64_t)pl.n_dtiles * kch_t)), dim3(256), 0, s, h + r0 * d,
+                         rows, d, kch_t, img_ht);
+    // dZ of the chunk from the recomputed logits (vocabulary strips as in scoring)
+    {
+      const ScorePlan sp = plan_score(rows, d, V);
+      ScoreParams pg{};
+      pg.a = img_w;
+      pg.b = img_h;
+      pg.n_chunks = (int)(2 * d / kChunk);
+      pg.V = (int)V;
+      pg.n_rows = (int)rows;
+      pg.n_vtiles = sp.n_vtiles;
+      pg.tiles_per_strip = sp.tiles_per_strip;
+      pg.n_strips = sp.n_strips;
+      pg.n_ttiles = sp.n_ttiles;
+      pg.n_tblocks = sp.n_tblocks;
+      pg.inv_temp = dsc.inv_temperature;
+      pg.ids = dsc.token_ids + r0;
+      pg.g_coef = dsc.coef;
+      pg.g_lse = dsc.lse;
+      pg.g_slot = dsc.row_slot ? dsc.row_slot + r0 : nullptr;
+      pg.g_slot_offset = r0;
+      pg.gz_t = img_zt;
+      pg.gz_v = img_zv;
+      pg.kch_v = pl.kch_v;
+      pg.kch_t = kch_t;
+      hipLaunchKernelGGL((score_kernel<kBF16, kEpiGrad>), dim3((unsigned)sp.grid), dim3(kThreads), 0, s, pg);
+    }
+    // dH[chunk] = dZ W: A = dZ (rows = tokens), B = W^T (rows = d), K = vocabulary
+    if (dh) {
+      ScoreParams pc{};
+      unsigned grid = 0;
+      gemm_grid(n_ttiles, pl.n_dtiles, pc, grid);
+      pc.a = img_zt;
+      pc.b = img_wt;
+      pc.n_chunks = pl.kch_v;
+      pc.n_rows = (int)d;
+      pc.V = (int)rows;
+      pc.c = dh + r0 * d;
+      pc.ldc = d;
+      pc.c_rows = (int)rows;
+      pc.c_accumulate = 0;
+      hipLaunchKernelGGL((score_kernel<kBF16, kEpiStore>), dim3(grid), dim3(kThreads), 0, s, pc);
+    }
+    // dW (+)= dZ^T H: A = dZ^T (rows = vocabulary), B = H^T (rows = d), K = tokens
+    if (dw) {
+      ScoreParams pc{};
+      unsigned grid = 0;
+      gemm_grid(pl.n_vtiles, pl.n_dtiles, pc, grid);
+      pc.a = img_zv;
+      pc.b = img_ht;
+      pc.n_chunks = kch_t;
+      pc.n_rows = (int)d;
+      pc.V = (int)V;
+      pc.c = dw;
+      pc.ldc = d;
+      pc.c_rows = (int)V;
+      pc.c_accumulate = (r0 > 0 || dsc.accumulate_dw) ? 1 : 0;
+      hipLaunchKernelGGL((score_kernel<kBF16, kEpiStore>), dim3(grid), dim3(kThreads), 0, s, pc);
+    }
+  }
   return hipGetLastError();
 }
 
@@ -1010,14 +1319,14 @@ hipError_t launch_sample(const acrl_sample_desc& dsc, const ScorePlan& pl, hipSt
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
     pm.a_mx = static_cast<const uint8_t*>(dsc.wq_scales);
     pm.b_mx = static_cast<const uint8_t*>(dsc.hq_scales);
-    hipLaunchKernelGGL((score_kernel<kMX, true>), dim3(grid), dim3(kThreads), 0, s, pm);
+    hipLaunchKernelGGL((score_kernel<kMX, kEpiSample>), dim3(grid), dim3(kThreads), 0, s, pm);
   } else {
     pm.a_scale = static_cast<const float*>(dsc.wq_scales);
     pm.b_scale = static_cast<const float*>(dsc.hq_scales);
     if (dsc.mu_scaling == ACRL_SCALE_PER_ROW)
-      hipLaunchKernelGGL((score_kernel<kFP8Row, true>), dim3(grid), dim3(kThreads), 0, s, pm);
+      hipLaunchKernelGGL((score_kernel<kFP8Row, kEpiSample>), dim3(grid), dim3(kThreads), 0, s, pm);
     else
-      hipLaunchKernelGGL((score_kernel<kFP8Tensor, true>), dim3(grid), dim3(kThreads), 0, s, pm);
+      hipLaunchKernelGGL((score_kernel<kFP8Tensor, kEpiSample>), dim3(grid), dim3(kThreads), 0, s, pm);
   }
   SampleMergeParams mp{};
   mp.n_rows = (int)dsc.n_rows;

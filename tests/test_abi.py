@@ -53,11 +53,12 @@ def test_exported_dynamic_symbols_match_header():
 
 def test_descriptor_layout_matches_binding():
     acrl = _acrl()
-    sizes = [ctypes.c_size_t() for _ in range(4)]
+    sizes = [ctypes.c_size_t() for _ in range(6)]
     acrl.lib().acrl_abi_struct_sizes(*[ctypes.byref(s) for s in sizes])
     assert [s.value for s in sizes] == [ctypes.sizeof(acrl.ScoreDesc), ctypes.sizeof(acrl.ReduceDesc),
-                                        ctypes.sizeof(acrl.ControllerDesc), ctypes.sizeof(acrl.SampleDesc)]
-    assert acrl.lib().acrl_abi_version() == 2
+                                        ctypes.sizeof(acrl.ControllerDesc), ctypes.sizeof(acrl.SampleDesc),
+                                        ctypes.sizeof(acrl.SurrogateDesc), ctypes.sizeof(acrl.BackwardDesc)]
+    assert acrl.lib().acrl_abi_version() == 3
 
 
 def test_status_strings():
@@ -140,3 +141,39 @@ def test_reference_from_groups_host_helper():
     assert abs(acrl.acrl_reference_from_groups([0.01, 0.5, 0.03], [8, 0, 8]) - 0.02) < 1e-8
     with pytest.raises(acrl.AcrlError):
         acrl.acrl_reference_from_groups([0.01], [0])
+
+
+def test_surrogate_rejects_bad_arguments():
+    acrl = _acrl()
+    L = acrl.lib()
+    buf = _fake(64)
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    ok = dict(B=2, L=4, n_groups=1, mask=p, group_of_seq=p, logp_new=p, logp_old=p, adv=p,
+              eps_low=0.2, eps_high=0.2, coef=p, loss=p, workspace=p, workspace_bytes=1 << 30)
+    for bad in (dict(B=-1), dict(n_groups=0), dict(eps_low=1.0), dict(eps_low=-0.1), dict(eps_high=-0.1),
+                dict(loss=None), dict(coef=None), dict(logp_old=None)):
+        d = acrl.SurrogateDesc(**{**ok, **bad})
+        assert L.acrl_surrogate(ctypes.byref(d), None) == acrl.ACRL_ERR_INVALID_ARG, bad
+    d = acrl.SurrogateDesc(**{**ok, "workspace_bytes": 1})
+    assert L.acrl_surrogate(ctypes.byref(d), None) == acrl.ACRL_ERR_WORKSPACE
+    nb = ctypes.c_size_t()
+    assert L.acrl_surrogate_workspace_size(64, 8, ctypes.byref(nb)) == 0 and nb.value >= 64 * 16
+
+
+def test_backward_rejects_bad_arguments():
+    acrl = _acrl()
+    L = acrl.lib()
+    buf = _fake(64)
+    p = ctypes.c_void_p(ctypes.addressof(buf) + (-ctypes.addressof(buf)) % 16)
+    ok = dict(n_rows=4, d=256, V=1000, h=p, w=p, token_ids=p, coef=p, lse=p, inv_temperature=1.0,
+              dh=p, dw=p, workspace=p, workspace_bytes=1 << 40)
+    for bad in (dict(d=100), dict(V=0), dict(V=1 << 23), dict(n_rows=-1), dict(inv_temperature=0.0),
+                dict(dh=None, dw=None), dict(lse=None), dict(coef=None), dict(token_chunk=-5)):
+        d = acrl.BackwardDesc(**{**ok, **bad})
+        assert L.acrl_lm_head_backward(ctypes.byref(d), None) == acrl.ACRL_ERR_INVALID_ARG, bad
+    d = acrl.BackwardDesc(**{**ok, "workspace_bytes": 16})
+    assert L.acrl_lm_head_backward(ctypes.byref(d), None) == acrl.ACRL_ERR_WORKSPACE
+    nb = ctypes.c_size_t()
+    assert L.acrl_backward_workspace_size(300, 256, 1000, 0, ctypes.byref(nb)) == 0
+    # W, W^T, H, H^T and the two dZ images of one 512-row chunk
+    assert nb.value >= 2 * (1024 * 256 * 2) + 2 * (512 * 256 * 2) + 2 * (512 * 1024 * 2)
