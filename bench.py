@@ -43,6 +43,8 @@ def main():
     ap.add_argument("--workload", default="q8b", choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the surrogate + LM-head backward leg")
     ap.add_argument("--counters", action="store_true",
                     help="copy calibration + one step only (for rocprofv3 --pmc passes)")
     args = ap.parse_args()
@@ -148,6 +150,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
         step()
+        if not args.no_backward:
+            backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv, 1.0, reps=0)
         torch.cuda.synchronize()
         log("counters run done")
         return
@@ -251,11 +255,64 @@ def main():
     }
 
     line["config"]["hbm_kernels"] = hbm_kernels(torch, acrl, dev, H, w)
+    if not args.no_backward:
+        line["backward"] = backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv,
+                                        X_ref[0])
 
     # ---------------- CPU baseline: the oracle on host cores, bounded sample
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, T, H, W, hq, hs, wq, ws, ids, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+
+
+def backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv, X, reps=2):
+    """The training side of the step, after scoring: the ACRL-weighted
+    surrogate's coefficients (from this batch's pi log-probs, the controller's
+    weights and the advantages; logp_old = logp_new, the first update of a
+    batch) and the LM-head backward dH = dZ W, dW = dZ^T H with dZ recomputed
+    from the logits.  Roofline: 3 x 2 T V d FLOP (logits, dH, dW) at the BF16
+    MFMA peak."""
+    d, V = w.d, w.V
+    sc = acrl.acrl_score_pi_mu(H, W, hq, hs, wq, ws, w.scaling, ids, inv_temperature=w.inv_temperature,
+                               out_slot=slots, n_slots=w.slots, want=("entropy", "lse"))
+    red = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, sc["logp_pi"], sc["logp_mu"], mask, groups,
+                                       entropy_pi=sc["entropy_pi"], entropy_mu=sc["entropy_mu"], want_d_tok=False)
+    _, weight = acrl.acrl_controller_step(w.B, w.L, w.n_prompts, mask, groups, sc["logp_pi"], sc["logp_mu"], adv,
+                                          False, acrl.Y_GROUP, red["seq_mean_d"], red["group_y"], red["stats"],
+                                          X, 0.65, 3.0, want_alpha=False)
+    dh = torch.empty((T, d), dtype=torch.float32, device=H.device)
+    dw = torch.empty((V, d), dtype=torch.float32, device=H.device)
+
+    def run():
+        coef, loss = acrl.acrl_surrogate(w.B, w.L, w.n_prompts, mask, groups, sc["logp_pi"], sc["logp_pi"], adv,
+                                         False, weight=weight)
+        acrl.acrl_lm_head_backward(H, W, ids, coef, sc["lse_pi"], inv_temperature=w.inv_temperature,
+                                   row_slot=slots, dh=dh, dw=dw)
+        return loss
+
+    run()
+    torch.cuda.synchronize()
+    if reps == 0:  # one untimed pass (counter collection)
+        return None
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        loss = run()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    flops = 3 * 2.0 * T * V * d
+    ach = flops / (ms * 1e-3) / 1e12
+    res = {"what": "acrl_surrogate + acrl_lm_head_backward (dH and dW) over the batch's valid tokens",
+           "ms": round(ms, 3), "tokens_per_s": round(T / (ms * 1e-3), 1),
+           "roofline": {"bound": "mfma", "achieved": round(ach, 1), "peak": PEAK_TFLOPS["bf16"],
+                        "unit": "TFLOP/s", "frac": round(ach / PEAK_TFLOPS["bf16"], 4),
+                        "flops": flops, "flops_rule": "3 x 2 T V d (logits recomputed, dH, dW)"},
+           "loss": float(loss.item()), "dw_abs_max": float(dw.abs().max().item())}
+    log("backward:", res)
+    del dh, dw
+    torch.cuda.empty_cache()
+    return res
 
 
 def hbm_kernels(torch, acrl, dev, H, w, reps=5):
