@@ -83,6 +83,10 @@ def lib() -> ctypes.CDLL:
         L.acrl_ref_token_stats.argtypes = [P, I64, ctypes.c_int32, P, P, P]
         L.acrl_ref_score.restype = I32
         L.acrl_ref_score.argtypes = [I64, I64, I64, P, P, P, P, P, P, I32, P, P, D] + [P] * 8
+        L.acrl_ref_token_divergence.restype = None
+        L.acrl_ref_token_divergence.argtypes = [P, P, I64, P, P, P]
+        L.acrl_ref_divergence.restype = I32
+        L.acrl_ref_divergence.argtypes = [I64, I64, I64, P, P, P, P, P, P, I32, P, D, P, P, P]
         L.acrl_ref_discrepancy_reduce.restype = I32
         L.acrl_ref_discrepancy_reduce.argtypes = [I64, I64, P, P, P, P, P, P, I64] + [P] * 8
         L.acrl_ref_controller_step.restype = I32
@@ -216,6 +220,32 @@ def score(h, w, hq, hq_scales, wq, wq_scales, scaling: int, ids, mask=None,
     _check(lib().acrl_ref_score(n_rows, d, V, _p(h), _p(w), _p(hq), _p(hs), _p(wq), _p(ws),
                                 scaling, _p(ids), _p(m), inv_temperature,
                                 *[_p(out[k]) for k in names]), "score")
+    return out
+
+
+def token_divergence(z_pi, z_mu):
+    """(KL(pi||mu), KL(mu||pi), Euclidean distance) of softmax(z_pi), softmax(z_mu)."""
+    zp = _c(z_pi, np.float64)
+    zm = _c(z_mu, np.float64)
+    out = np.zeros(3, np.float64)
+    lib().acrl_ref_token_divergence(_p(zp), _p(zm), zp.size, _p(out[0:1]), _p(out[1:2]), _p(out[2:3]))
+    return float(out[0]), float(out[1]), float(out[2])
+
+
+def divergence(h, w, hq, hq_scales, wq, wq_scales, scaling: int, mask=None,
+               inv_temperature: float = 1.0) -> dict:
+    """Full-vocabulary KL(pi||mu), KL(mu||pi) and Euclidean distance of every row."""
+    h, w = _c(h, np.uint16), _c(w, np.uint16)
+    hq, wq = _c(hq, np.uint8), _c(wq, np.uint8)
+    n_rows, d = h.shape
+    V = w.shape[0]
+    sdt = np.uint8 if scaling == MX32 else np.float32
+    hs, ws = _c(hq_scales, sdt), _c(wq_scales, sdt)
+    m = None if mask is None else _c(mask, np.uint8)
+    out = {k: np.zeros(n_rows, np.float64) for k in ("kl_pi_mu", "kl_mu_pi", "l2")}
+    _check(lib().acrl_ref_divergence(n_rows, d, V, _p(h), _p(w), _p(hq), _p(hs), _p(wq), _p(ws), scaling,
+                                     _p(m), inv_temperature, _p(out["kl_pi_mu"]), _p(out["kl_mu_pi"]),
+                                     _p(out["l2"])), "divergence")
     return out
 
 

@@ -286,6 +286,31 @@ static const void* row_scale_ptr(const void* hq_scales, int scaling, int64_t r, 
   return (const uint8_t*)hq_scales + r * (d / 32);
 }
 
+static double ref_lse(const double* z, int64_t V) {
+  double m = z[0];
+  for (int64_t v = 1; v < V; ++v)
+    if (z[v] > m) m = z[v];
+  double s = 0.0;
+  for (int64_t v = 0; v < V; ++v) s += exp(z[v] - m);
+  return m + log(s);
+}
+
+void acrl_ref_token_divergence(const double* z_pi, const double* z_mu, int64_t V,
+                               double* kl_pi_mu, double* kl_mu_pi, double* l2) {
+  const double lp = ref_lse(z_pi, V), lm = ref_lse(z_mu, V);
+  double a = 0.0, b = 0.0, c = 0.0;
+  for (int64_t v = 0; v < V; ++v) {
+    const double log_p = z_pi[v] - lp, log_q = z_mu[v] - lm;
+    const double p = exp(log_p), q = exp(log_q);
+    a += p * (log_p - log_q);
+    b += q * (log_q - log_p);
+    c += (p - q) * (p - q);
+  }
+  if (kl_pi_mu) *kl_pi_mu = a;
+  if (kl_mu_pi) *kl_mu_pi = b;
+  if (l2) *l2 = sqrt(c);
+}
+
 int acrl_ref_score(int64_t n_rows, int64_t d, int64_t V,
                    const uint16_t* h, const uint16_t* w,
                    const uint8_t* hq, const void* hq_scales,
@@ -733,4 +758,41 @@ int acrl_ref_lm_head_backward(int64_t n_rows, int64_t d, int64_t V, const uint16
   }
   free(dz);
   return 0;
+}
+
+int acrl_ref_divergence(int64_t n_rows, int64_t d, int64_t V, const uint16_t* h, const uint16_t* w,
+                        const uint8_t* hq, const void* hq_scales, const uint8_t* wq,
+                        const void* wq_scales, int scaling, const uint8_t* mask,
+                        double inv_temperature, double* kl_pi_mu, double* kl_mu_pi, double* l2) {
+  if (n_rows < 0 || d <= 0 || V <= 0 || !h || !w || !hq || !hq_scales || !wq || !wq_scales)
+    return -1;
+  if (scaling != REF_PER_TENSOR && scaling != REF_PER_ROW && scaling != REF_MX32) return -1;
+  if (scaling == REF_MX32 && d % 32 != 0) return -1;
+  int bad = 0;
+#pragma omp parallel reduction(| : bad)
+  {
+    double* zp = (double*)malloc((size_t)V * sizeof(double));
+    double* zm = (double*)malloc((size_t)V * sizeof(double));
+    if (!zp || !zm) bad = 1;
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t r = 0; r < n_rows; ++r) {
+      if (bad) continue;
+      double a = 0.0, b = 0.0, c = 0.0;
+      if (!mask || mask[r]) {
+        if (acrl_ref_logits_pi(h + r * d, w, d, V, inv_temperature, zp) ||
+            acrl_ref_logits_mu(hq + r * d, row_scale_ptr(hq_scales, scaling, r, d), wq, wq_scales,
+                               scaling, d, V, inv_temperature, zm)) {
+          bad = 1;
+          continue;
+        }
+        acrl_ref_token_divergence(zp, zm, V, &a, &b, &c);
+      }
+      if (kl_pi_mu) kl_pi_mu[r] = a;
+      if (kl_mu_pi) kl_mu_pi[r] = b;
+      if (l2) l2[r] = c;
+    }
+    free(zp);
+    free(zm);
+  }
+  return bad ? -1 : 0;
 }

@@ -96,6 +96,25 @@ int acrl_ref_score(int64_t n_rows, int64_t d, int64_t V,
                    double* logp_pi, double* logp_mu, double* ent_pi, double* ent_mu,
                    double* lse_pi, double* lse_mu, double* z_pi, double* z_mu);
 
+/* ---- Full-vocabulary discrepancy between the two policies --------------- *
+ * The paper measures the discrepancy on the sampled token's probabilities
+ * (Eq. distance_metric) and names the KL divergence and the Euclidean
+ * distance as other measures (remark after Eq. distance_metric; Sec. 6).
+ * Over the whole vocabulary, with p = softmax(z_pi), q = softmax(z_mu):
+ *   kl_pi_mu = sum_v p_v (log p_v - log q_v)    (KL(pi || mu))
+ *   kl_mu_pi = sum_v q_v (log q_v - log p_v)    (KL(mu || pi))
+ *   l2       = sqrt(sum_v (p_v - q_v)^2)         (Euclidean distance)
+ * in double: the two log-sum-exps first, then the sums over v.  Any output
+ * may be NULL.                                                              */
+void acrl_ref_token_divergence(const double* z_pi, const double* z_mu, int64_t V,
+                               double* kl_pi_mu, double* kl_mu_pi, double* l2);
+/* The same for every row, from the logits of acrl_ref_score (same operands
+ * and arguments); rows with mask[r] == 0 get 0.                            */
+int acrl_ref_divergence(int64_t n_rows, int64_t d, int64_t V, const uint16_t* h, const uint16_t* w,
+                        const uint8_t* hq, const void* hq_scales, const uint8_t* wq,
+                        const void* wq_scales, int scaling, const uint8_t* mask,
+                        double inv_temperature, double* kl_pi_mu, double* kl_mu_pi, double* l2);
+
 /* ---- a6/a7: per-token discrepancy and the segmented masked reduce ------ *
  * Slot (i, j) = i*L + j.  ent_pi/ent_mu may be NULL (means reported as 0).
  * Outputs: d_tok[B*L] (0 where masked), seq_len[B], seq_sum_d[B],
