@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ACRL_ABI_VERSION 3
+#define ACRL_ABI_VERSION 4
 
 typedef int acrl_status;
 enum {
@@ -149,6 +149,17 @@ acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, vo
  * given, becomes nonzero; the flag is never cleared by the library).
  * The workspace holds a tiled copy of W, h, Wq and hq (about 3 (V + n_rows) d
  * bytes) besides the per-strip partial states.
+ *
+ * Full-vocabulary measures (optional; the paper's measure is the absolute
+ * distance on the sampled token, Eq. distance_metric, and it names the KL
+ * divergence and the Euclidean distance as the others): with p = softmax of
+ * pi's logits and q = softmax of mu's over the whole vocabulary,
+ *   kl_pi_mu = sum_v p_v log(p_v / q_v),  kl_mu_pi = sum_v q_v log(q_v / p_v),
+ *   l2 = sqrt(sum_v (p_v - q_v)^2),
+ * per row (0 for masked rows).  When any of the three is non-NULL, pi's
+ * logits of div_chunk rows at a time (0 = 16384) are kept in the workspace
+ * (4 bytes per logit) between the pi and mu kernels, and the workspace must
+ * have acrl_score_div_workspace_size() bytes.
  */
 typedef struct acrl_score_desc {
   int64_t n_rows;               /* rows scored by this call (a chunk of the batch is fine) */
@@ -176,10 +187,17 @@ typedef struct acrl_score_desc {
   int32_t* error_flag;          /* device int, nullable                                     */
   void* workspace;              /* acrl_score_workspace_size() bytes, device                */
   size_t workspace_bytes;
+  float* kl_pi_mu;              /* [slots] out, nullable: KL(pi || mu) over the vocabulary   */
+  float* kl_mu_pi;              /* [slots] out, nullable: KL(mu || pi)                       */
+  float* l2;                    /* [slots] out, nullable: Euclidean distance of p and q      */
+  int64_t div_chunk;            /* rows per pass of the three measures (0 = 16384)           */
 } acrl_score_desc;
 
 acrl_status acrl_score_workspace_size(int64_t n_rows, int64_t d, int64_t V, int mu_scaling,
                                       size_t* bytes);
+/* Workspace of a call that also asks for the full-vocabulary measures.      */
+acrl_status acrl_score_div_workspace_size(int64_t n_rows, int64_t d, int64_t V, int mu_scaling,
+                                          int64_t div_chunk, size_t* bytes);
 acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream);
 
 /* ======================================================================== */

@@ -29,7 +29,7 @@ STAT_NAMES = ["y_batch", "tok_mean_d", "tok_max_d", "tok_std_d", "mean_h_pi", "m
 EXPORTED = [
     "acrl_status_string", "acrl_last_error", "acrl_abi_version", "acrl_abi_struct_sizes",
     "acrl_quantize_workspace_size", "acrl_quantize_fp8", "acrl_fp8_encode",
-    "acrl_score_workspace_size", "acrl_score_pi_mu", "acrl_trace_score_events",
+    "acrl_score_workspace_size", "acrl_score_div_workspace_size", "acrl_score_pi_mu", "acrl_trace_score_events",
     "acrl_reduce_workspace_size", "acrl_discrepancy_reduce",
     "acrl_controller_step", "acrl_reference_from_groups", "acrl_sample_mu",
     "acrl_surrogate_workspace_size", "acrl_surrogate",
@@ -50,7 +50,8 @@ class ScoreDesc(ctypes.Structure):
                 ("token_ids", _P), ("mask", _P), ("out_slot", _P),
                 ("logp_pi", _P), ("logp_mu", _P), ("entropy_pi", _P), ("entropy_mu", _P),
                 ("lse_pi", _P), ("lse_mu", _P), ("logit_pi", _P), ("logit_mu", _P),
-                ("error_flag", _P), ("workspace", _P), ("workspace_bytes", _SZ)]
+                ("error_flag", _P), ("workspace", _P), ("workspace_bytes", _SZ),
+                ("kl_pi_mu", _P), ("kl_mu_pi", _P), ("l2", _P), ("div_chunk", _I64)]
 
 
 class ReduceDesc(ctypes.Structure):
@@ -129,6 +130,8 @@ def lib() -> ctypes.CDLL:
         L.acrl_fp8_encode.argtypes = [_P, _I64, _I32, _P, _P]
         L.acrl_score_workspace_size.restype = _I32
         L.acrl_score_workspace_size.argtypes = [_I64, _I64, _I64, _I32, ctypes.POINTER(_SZ)]
+        L.acrl_score_div_workspace_size.restype = _I32
+        L.acrl_score_div_workspace_size.argtypes = [_I64, _I64, _I64, _I32, _I64, ctypes.POINTER(_SZ)]
         L.acrl_score_pi_mu.restype = _I32
         L.acrl_score_pi_mu.argtypes = [ctypes.POINTER(ScoreDesc), _P]
         L.acrl_trace_score_events.restype = _I32
@@ -236,11 +239,12 @@ def acrl_fp8_encode(x: torch.Tensor, rounding: int = ROUND_NEAREST_EVEN, q=None,
 def acrl_score_pi_mu(h, w, hq, hq_scales, wq, wq_scales, mu_scaling: int, token_ids,
                      inv_temperature: float = 1.0, mask=None, out_slot=None, n_slots=None,
                      outputs: Optional[dict] = None, want=("entropy", "lse", "logit"),
-                     error_flag=None, stream=None) -> dict:
+                     error_flag=None, stream=None, divergence: bool = False, div_chunk: int = 0) -> dict:
     """Score every row of h under pi (bf16) and mu (fp8/mxfp8).
 
     Returns a dict of float32 [n_slots] tensors: logp_pi, logp_mu and, per
-    `want`, entropy_pi/mu, lse_pi/mu, logit_pi/mu.  Pass `outputs` to reuse
+    `want`, entropy_pi/mu, lse_pi/mu, logit_pi/mu; with divergence=True also
+    the full-vocabulary kl_pi_mu, kl_mu_pi and l2.  Pass `outputs` to reuse
     preallocated tensors."""
     _dev(h, torch.bfloat16, "h")
     _dev(w, torch.bfloat16, "w")
@@ -256,12 +260,18 @@ def acrl_score_pi_mu(h, w, hq, hq_scales, wq, wq_scales, mu_scaling: int, token_
     names = ["logp_pi", "logp_mu"]
     for k in want:
         names += [k + "_pi", k + "_mu"]
+    if divergence:
+        names += ["kl_pi_mu", "kl_mu_pi", "l2"]
     for k in names:
         if k not in out:
             out[k] = torch.zeros(n_slots, dtype=torch.float32, device=dev)
     nb = _SZ()
-    _check(lib().acrl_score_workspace_size(n_rows, d, V, mu_scaling, ctypes.byref(nb)),
-           "acrl_score_workspace_size")
+    if divergence:
+        _check(lib().acrl_score_div_workspace_size(n_rows, d, V, mu_scaling, int(div_chunk), ctypes.byref(nb)),
+               "acrl_score_div_workspace_size")
+    else:
+        _check(lib().acrl_score_workspace_size(n_rows, d, V, mu_scaling, ctypes.byref(nb)),
+               "acrl_score_workspace_size")
     ws = _workspace(nb.value, dev)
     desc = ScoreDesc(n_rows=n_rows, d=d, V=V, h=_ptr(h), w=_ptr(w), hq=_ptr(hq),
                      hq_scales=_ptr(hq_scales), wq=_ptr(wq), wq_scales=_ptr(wq_scales),
@@ -271,7 +281,10 @@ def acrl_score_pi_mu(h, w, hq, hq_scales, wq, wq_scales, mu_scaling: int, token_
                      entropy_pi=_ptr(out.get("entropy_pi")), entropy_mu=_ptr(out.get("entropy_mu")),
                      lse_pi=_ptr(out.get("lse_pi")), lse_mu=_ptr(out.get("lse_mu")),
                      logit_pi=_ptr(out.get("logit_pi")), logit_mu=_ptr(out.get("logit_mu")),
-                     error_flag=_ptr(error_flag), workspace=_ptr(ws), workspace_bytes=nb.value)
+                     error_flag=_ptr(error_flag), workspace=_ptr(ws), workspace_bytes=nb.value,
+                     kl_pi_mu=_ptr(out.get("kl_pi_mu") if divergence else None),
+                     kl_mu_pi=_ptr(out.get("kl_mu_pi") if divergence else None),
+                     l2=_ptr(out.get("l2") if divergence else None), div_chunk=int(div_chunk))
     _check(lib().acrl_score_pi_mu(ctypes.byref(desc), _stream(stream)), "acrl_score_pi_mu")
     return out
 

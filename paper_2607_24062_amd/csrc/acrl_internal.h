@@ -34,9 +34,13 @@ struct ScorePlan {
   size_t ws_logit_offset[2]; // byte offsets of the sampled-token logits of pi / mu
   size_t ws_pack_offset[4];  // byte offsets of the packed W, H (bf16) and Wq, Hq (e4m3)
   size_t ws_best_offset;     // sampling: the strips' best key, logit and row
+  int div_tiles;             // full-vocabulary measures: token tiles per pass (0 = not planned)
+  size_t ws_zbuf_offset[2];  //   the logits of pi and mu of one pass
   size_t ws_bytes;
 };
-ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V);
+// div_rows > 0 plans the full-vocabulary measures in passes of div_rows rows.
+ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows = 0);
+constexpr int64_t kDivergenceChunk = 16384;  // default rows per pass of the full-vocabulary measures
 // Events recorded around the score kernels (tracing hook), per thread.
 void set_score_trace(void* const* events, int n);
 hipError_t launch_score(const acrl_score_desc& desc, const ScorePlan& plan, hipStream_t s);

@@ -214,10 +214,22 @@ acrl_status acrl_score_workspace_size(int64_t n_rows, int64_t d, int64_t V, int 
   return ACRL_OK;
 }
 
+acrl_status acrl_score_div_workspace_size(int64_t n_rows, int64_t d, int64_t V, int mu_scaling, int64_t div_chunk,
+                                          size_t* bytes) {
+  acrl_status st = acrl_score_workspace_size(n_rows, d, V, mu_scaling, bytes);
+  if (st != ACRL_OK) return st;
+  ACRL_REQUIRE(div_chunk >= 0 && div_chunk <= ((int64_t)1 << 24), "div_chunk must lie in [0, 2^24]");
+  *bytes = acrl::plan_score(n_rows, d, V, div_chunk > 0 ? div_chunk : acrl::kDivergenceChunk).ws_bytes;
+  return ACRL_OK;
+}
+
 acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream) {
   acrl_status st = acrl::validate_score(desc);
   if (st != ACRL_OK) return st;
-  const acrl::ScorePlan plan = acrl::plan_score(desc->n_rows, desc->d, desc->V);
+  const bool div = desc->kl_pi_mu || desc->kl_mu_pi || desc->l2;
+  ACRL_REQUIRE(desc->div_chunk >= 0 && desc->div_chunk <= ((int64_t)1 << 24), "div_chunk must lie in [0, 2^24]");
+  const acrl::ScorePlan plan = acrl::plan_score(
+      desc->n_rows, desc->d, desc->V, div ? (desc->div_chunk > 0 ? desc->div_chunk : acrl::kDivergenceChunk) : 0);
   if (desc->n_rows > 0 && (!desc->workspace || desc->workspace_bytes < plan.ws_bytes)) {
     set_error("acrl_score_pi_mu needs %zu workspace bytes, got %zu", plan.ws_bytes, desc->workspace_bytes);
     return ACRL_ERR_WORKSPACE;

@@ -45,6 +45,7 @@ enum Epilogue {
   kEpiSample = 1,   // the same plus a Gumbel-max draw (sampling from mu)
   kEpiGrad = 2,     // dZ = coef (onehot - softmax) / tau as bf16 operand images (backward)
   kEpiStore = 3,    // the product tile itself, fp32, stored (optionally on top of C)
+  kEpiSoftmaxZ = 4, // kEpiSoftmax + the tile's logits stored (full-vocabulary measures)
 };
 
 constexpr int kTileV = 256;            // vocabulary rows per workgroup tile
@@ -103,6 +104,10 @@ struct ScoreParams {
   int64_t ldc;
   int c_rows;              // valid A rows (M)
   int c_accumulate;        // 1: C += product (C is read once before the K loop)
+  // row chunks and the full-vocabulary measures (kEpiSoftmaxZ)
+  int tt_offset;           // token tile of this launch's tile 0 (n_ttiles counts the launch's tiles)
+  float* zbuf;             // logits of the launch's rows, row-major [256 n_ttiles][z_ld] (natural units)
+  int64_t z_ld;
 };
 
 // Philox4x32-10 (Salmon et al., SC 2011): 10 rounds on a 128-bit counter
@@ -226,7 +231,7 @@ template <int MODE, int EPI>
 __global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
 void score_kernel(ScoreParams p) {
   constexpr bool SAMPLE = EPI == kEpiSample;
-  constexpr bool SOFTMAX = EPI == kEpiSoftmax || EPI == kEpiSample;
+  constexpr bool SOFTMAX = EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ;
   static_assert(MODE == kBF16 || SOFTMAX, "the backward epilogues take bf16 operands");
   constexpr int NS = Pipe<MODE>::kStages;
   constexpr int SB = Pipe<MODE>::kScaleBytes;
@@ -251,7 +256,8 @@ void score_kernel(ScoreParams p) {
     st = (blk / p.n_tblocks) * kBlockS + k % kBlockS;
   }
   if (tt >= p.n_ttiles || st >= p.n_strips) return;  // padding of the grid
-  const int t0 = tt * kTileT;
+  const int ttg = tt + p.tt_offset;  // token tile in the whole call
+  const int t0 = ttg * kTileT;
   const int vt_begin = st * p.tiles_per_strip;
   const int vt_end = min(vt_begin + p.tiles_per_strip, p.n_vtiles);
   const int n_iter = (vt_end - vt_begin) * p.n_chunks;
@@ -267,7 +273,7 @@ void score_kernel(ScoreParams p) {
   for (int j = 0; j < 4; ++j) {
     tok[j] = t0 + wt * 128 + j * 32 + r32;
     const int tc = min(tok[j], p.n_rows - 1);
-    id[j] = (EPI == kEpiSoftmax || EPI == kEpiGrad) ? p.ids[tc] : -1;
+    id[j] = (EPI == kEpiSample || EPI == kEpiStore) ? -1 : p.ids[tc];
     gl2[j] = 0.0f;
     gc[j] = 0.0f;
     if constexpr (EPI == kEpiGrad) {
@@ -324,7 +330,7 @@ void score_kernel(ScoreParams p) {
   const uint32_t lane_off = (uint32_t)lane * 16;
   const uint32_t tile_bytes = (uint32_t)p.n_chunks * kPackBlock;  // packed bytes of one tile
   const int b_rows = min(kTileT, p.n_rows - t0);  // valid rows of the token tile
-  const __amdgpu_buffer_rsrc_t rsrc_b = make_rsrc(p.b + (int64_t)tt * tile_bytes, tile_bytes);
+  const __amdgpu_buffer_rsrc_t rsrc_b = make_rsrc(p.b + (int64_t)ttg * tile_bytes, tile_bytes);
   auto stage_at = [&](int stg) { return lds + stg * kStageBytes; };
   auto scales_at = [&](int stg) { return lds + NS * kStageBytes + stg * SB; };
   auto rowscales_at = [&](int q) {  // FP8 per-row: weight-row scales of tile q
@@ -489,6 +495,15 @@ void score_kernel(ScoreParams p) {
             v[i] = acc_read(acc[b][j][i]);
             if constexpr (MODE == kFP8Row) v[i] *= rs[i];
           }
+          if constexpr (EPI == kEpiSoftmaxZ) {
+            // the logits z = acc * scale (natural units) of the lane's token
+            // row: 4 runs of 4 consecutive vocabulary entries (16 bytes each)
+            float* zr = p.zbuf + (int64_t)(tt * kTileT + wt * 128 + j * 32 + r32) * p.z_ld + v0 + 32 * b + 4 * g;
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq)
+              *reinterpret_cast<f32x4*>(zr + 8 * qq) =
+                  f32x4{v[4 * qq] * cz[j], v[4 * qq + 1] * cz[j], v[4 * qq + 2] * cz[j], v[4 * qq + 3] * cz[j]};
+          }
           float mx[8];
 #pragma unroll
           for (int i = 0; i < 8; ++i) mx[i] = fmaxf(v[2 * i], v[2 * i + 1]);
@@ -571,6 +586,7 @@ void score_kernel(ScoreParams p) {
     };
     if (partial) run(std::true_type{});
     else run(std::false_type{});
+    if constexpr (EPI == kEpiSoftmaxZ) wait_vmcnt<0>();  // stores must not count in the pipeline's waits
   };
 
   // Backward (kEpiGrad): dZ[t, v] = coef_t (delta(v, a_t) - p_tv) / tau of the
@@ -838,6 +854,7 @@ void score_kernel(ScoreParams p) {
           p.best_logit[o] = bz[j];
           p.best_id[o] = bi[j];
         }
+
       }
     }
   }
@@ -899,6 +916,86 @@ __global__ __launch_bounds__(256) void pack_t_kernel(const uint16_t* __restrict_
 __global__ __launch_bounds__(256) void fill_zero_kernel(float* __restrict__ p, int64_t n) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
     p[i] = 0.0f;
+}
+
+// lse of row r in log2 units (M + log2 S) from the strips' (M, S, U) states.
+__device__ __forceinline__ float merged_lse2(const float* part, int64_t plane, int n_strips, int n_rows, int r) {
+  float M = kInitMax, S = 0.f, U = 0.f;
+  for (int s = 0; s < n_strips; ++s) {
+    const int64_t o = (int64_t)s * n_rows + r;
+    merge_state(M, S, U, part[o], part[plane + o], part[2 * plane + o]);
+  }
+  return M + log2f(S);
+}
+
+struct DivParams {
+  int n_rows;              // rows of the whole call
+  int n_strips;
+  int V;
+  int r0;                  // first row of this pass (row r0 + k is row k of the stored logits)
+  int64_t z_ld;
+  const float* z[2];       // logits of the pass's rows, pi and mu
+  const float* part[2];    // the strips' (M, S, U) states of pi and mu
+  const uint8_t* mask;
+  const int32_t* out_slot;
+  float* kl_pm;            // [slots] KL(pi || mu), nullable
+  float* kl_mp;            // [slots] KL(mu || pi), nullable
+  float* l2;               // [slots] Euclidean distance, nullable
+};
+
+// Full-vocabulary measures of one row per workgroup, from the stored logits
+// of both policies and their log-sum-exps A (log2 units): p = 2^(z_pi log2e
+// - A_pi), q likewise, and the log-ratio l_p - l_q formed as
+// (z_pi - z_mu) - (A_pi - A_mu) ln 2 so that its terms are small (and exactly
+// 0 for identical policies, whatever the compiler fuses):
+// KL(pi||mu) = sum p (l_p - l_q), KL(mu||pi) = sum q (l_q - l_p),
+// |p - q|_2 = sqrt(sum (p - q)^2).  fp32 sums per thread, then a fixed tree.
+__global__ __launch_bounds__(256) void divergence_kernel(DivParams p) {
+  const int k = blockIdx.x;
+  const int r = p.r0 + k;
+  const int64_t plane = (int64_t)p.n_strips * p.n_rows;
+  const bool active = p.mask ? p.mask[r] != 0 : true;
+  float a = 0.f, b = 0.f, c = 0.f;
+  if (active) {
+    const float ap = merged_lse2(p.part[0], plane, p.n_strips, p.n_rows, r);
+    const float aq = merged_lse2(p.part[1], plane, p.n_strips, p.n_rows, r);
+    const float dl = (ap - aq) * kLn2;
+    const float* zp = p.z[0] + (int64_t)k * p.z_ld;
+    const float* zq = p.z[1] + (int64_t)k * p.z_ld;
+    for (int v = threadIdx.x * 4; v < p.V; v += 1024) {
+      const f32x4 x = *reinterpret_cast<const f32x4*>(zp + v);
+      const f32x4 y = *reinterpret_cast<const f32x4*>(zq + v);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if (v + i < p.V) {
+          const float pr = fast_exp2(fmaf(x[i], kLog2e, -ap));
+          const float qr = fast_exp2(fmaf(y[i], kLog2e, -aq));
+          const float lr = (x[i] - y[i]) - dl;  // l_p - l_q
+          a = fmaf(pr, lr, a);
+          b = fmaf(-qr, lr, b);
+          c = fmaf(pr - qr, pr - qr, c);
+        }
+      }
+    }
+  }
+  __shared__ float sh[3][256];
+  sh[0][threadIdx.x] = a;
+  sh[1][threadIdx.x] = b;
+  sh[2][threadIdx.x] = c;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+#pragma unroll
+      for (int q = 0; q < 3; ++q) sh[q][threadIdx.x] += sh[q][threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const int slot = p.out_slot ? p.out_slot[r] : r;
+    if (p.kl_pm) p.kl_pm[slot] = sh[0][0];
+    if (p.kl_mp) p.kl_mp[slot] = sh[1][0];
+    if (p.l2) p.l2[slot] = sqrtf(sh[2][0]);
+  }
 }
 
 struct MergeParams {
@@ -1001,7 +1098,7 @@ void set_score_trace(void* const* events, int n) {
   for (int k = 0; k < 4; ++k) g_trace[k] = g_trace_on ? (hipEvent_t)events[k] : nullptr;
 }
 
-ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V) {
+ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows) {
   ScorePlan pl{};
   pl.n_ttiles = (int)((n_rows + kTileT - 1) / kTileT);
   pl.n_vtiles = (int)((V + kTileV - 1) / kTileV);
@@ -1055,6 +1152,19 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V) {
     pl.ws_pack_offset[q] = off;
     off += align_up(pack_bytes[q], 256);
   }
+  // full-vocabulary measures: the logits of both policies for one pass of
+  // div_tiles token tiles, row-major with the padded vocabulary as stride
+  pl.div_tiles = 0;
+  if (div_rows > 0) {
+    const int64_t rows = std::min<int64_t>((div_rows + kTileT - 1) / kTileT * kTileT,
+                                           (int64_t)pl.n_ttiles * kTileT);
+    pl.div_tiles = (int)std::max<int64_t>(rows / kTileT, 1);
+    const size_t zb = (size_t)pl.div_tiles * kTileT * pl.n_vtiles * kTileV * sizeof(float);
+    pl.ws_zbuf_offset[0] = off;
+    off += zb;
+    pl.ws_zbuf_offset[1] = off;
+    off += zb;
+  }
   pl.ws_bytes = off;
   return pl;
 }
@@ -1094,9 +1204,6 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   pp.n_chunks = (int)(2 * dsc.d / kChunk);
   pp.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[0]);
   pp.logit = reinterpret_cast<float*>(ws + pl.ws_logit_offset[0]);
-  trace(0, s);
-  hipLaunchKernelGGL((score_kernel<kBF16, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pp);
-  trace(1, s);
 
   // mu: e4m3 operands
   ScoreParams pm = pp;
@@ -1108,14 +1215,68 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
     pm.a_mx = static_cast<const uint8_t*>(dsc.wq_scales);
     pm.b_mx = static_cast<const uint8_t*>(dsc.hq_scales);
-    hipLaunchKernelGGL((score_kernel<kMX, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pm);
   } else {
     pm.a_scale = static_cast<const float*>(dsc.wq_scales);
     pm.b_scale = static_cast<const float*>(dsc.hq_scales);
-    if (dsc.mu_scaling == ACRL_SCALE_PER_ROW)
-      hipLaunchKernelGGL((score_kernel<kFP8Row, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pm);
+  }
+  auto launch_mu = [&](const ScoreParams& q, unsigned g, auto epi_tag) {
+    constexpr int E = decltype(epi_tag)::value;
+    if (dsc.mu_scaling == ACRL_SCALE_MX32)
+      hipLaunchKernelGGL((score_kernel<kMX, E>), dim3(g), dim3(kThreads), 0, s, q);
+    else if (dsc.mu_scaling == ACRL_SCALE_PER_ROW)
+      hipLaunchKernelGGL((score_kernel<kFP8Row, E>), dim3(g), dim3(kThreads), 0, s, q);
     else
-      hipLaunchKernelGGL((score_kernel<kFP8Tensor, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pm);
+      hipLaunchKernelGGL((score_kernel<kFP8Tensor, E>), dim3(g), dim3(kThreads), 0, s, q);
+  };
+  const bool div = dsc.kl_pi_mu || dsc.kl_mu_pi || dsc.l2;
+  trace(0, s);
+  if (!div) {
+    hipLaunchKernelGGL((score_kernel<kBF16, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pp);
+    trace(1, s);
+    launch_mu(pm, grid, std::integral_constant<int, kEpiSoftmax>{});
+  } else {
+    // passes of div_tiles token tiles: pi and mu (softmax + the logits
+    // stored), then the measures of the pass's rows
+    float* zbuf[2] = {reinterpret_cast<float*>(ws + pl.ws_zbuf_offset[0]),
+                      reinterpret_cast<float*>(ws + pl.ws_zbuf_offset[1])};
+    const int64_t z_ld = (int64_t)pl.n_vtiles * kTileV;
+    for (int tt0 = 0; tt0 < pl.n_ttiles; tt0 += pl.div_tiles) {
+      const int nt = std::min(pl.div_tiles, pl.n_ttiles - tt0);
+      const int ntb = (nt + kBlockT - 1) / kBlockT;
+      const unsigned g = (unsigned)((ntb * pl.n_sblocks + kXcds - 1) / kXcds * kXcds * kBlockT * kBlockS);
+      ScoreParams pz = pp;
+      pz.tt_offset = tt0;
+      pz.n_ttiles = nt;
+      pz.n_tblocks = ntb;
+      pz.zbuf = zbuf[0];
+      pz.z_ld = z_ld;
+      hipLaunchKernelGGL((score_kernel<kBF16, kEpiSoftmaxZ>), dim3(g), dim3(kThreads), 0, s, pz);
+      ScoreParams pq = pm;
+      pq.tt_offset = tt0;
+      pq.n_ttiles = nt;
+      pq.n_tblocks = ntb;
+      pq.zbuf = zbuf[1];
+      pq.z_ld = z_ld;
+      launch_mu(pq, g, std::integral_constant<int, kEpiSoftmaxZ>{});
+      DivParams dp{};
+      dp.n_rows = (int)dsc.n_rows;
+      dp.n_strips = pl.n_strips;
+      dp.V = (int)dsc.V;
+      dp.r0 = tt0 * kTileT;
+      dp.z_ld = z_ld;
+      dp.z[0] = zbuf[0];
+      dp.z[1] = zbuf[1];
+      dp.part[0] = pp.part;
+      dp.part[1] = pm.part;
+      dp.mask = dsc.mask;
+      dp.out_slot = dsc.out_slot;
+      dp.kl_pm = dsc.kl_pi_mu;
+      dp.kl_mp = dsc.kl_mu_pi;
+      dp.l2 = dsc.l2;
+      const int rows = (int)std::min<int64_t>(dsc.n_rows - dp.r0, (int64_t)nt * kTileT);
+      hipLaunchKernelGGL(divergence_kernel, dim3((unsigned)rows), dim3(256), 0, s, dp);
+    }
+    trace(1, s);
   }
 
   trace(2, s);

@@ -1,0 +1,159 @@
+"""GPU parity of the full-vocabulary measures of acrl_score_pi_mu (KL in
+both directions and the Euclidean distance between softmax(z_pi) and
+softmax(z_mu)) with the oracle.
+
+Bound.  If every GPU logit is within delta of the exact one, then to first
+order (the changes of the lse are p- resp. q-weighted means of the logit
+changes): |dKL| <= 2 delta |p - q|_1 <= 2 delta sqrt(2 KL) (Pinsker), and
+|dL2| <= |p (dz_pi - E_p dz_pi)|_2 + |q (dz_mu - E_q dz_mu)|_2
+      <= 2 delta (|p|_2 + |q|_2).
+The pi logits (BF16 MFMA, fp32 accumulation) are within ~1e-6 of the exact
+sums at these shapes; the mu logits come from the FP8 MFMA, whose sums of
+exact e4m3 products land up to ~1.6e-4 from the exact value at d = 256
+(the logit_mu output against the oracle's z_mu), growing like sqrt(d): so
+delta = 2e-4 sqrt(d / 256), and 1e-6 absolute for the final fp32 sums."""
+import math
+
+import numpy as np
+import pytest
+from scipy.special import softmax
+
+import inputs
+import oracle
+from cases import lossless_integer_case, random_bf16
+from gpu_util import down, torch_dev, up, up_bf16
+
+pytestmark = pytest.mark.gpu
+
+
+def _norms(H, W, hq, hs, wq, ws, scaling, tau, rows):
+    """|p|_2 and |q|_2 of the rows, from the oracle's logits."""
+    npn, nqn = [], []
+    for r in rows:
+        zp = oracle.logits_pi(H[r], W, 1.0 / tau)
+        zm = oracle.logits_mu(hq[r], oracle._row_scale(hs, scaling, r), wq, ws, scaling, 1.0 / tau)
+        npn.append(np.linalg.norm(softmax(zp)))
+        nqn.append(np.linalg.norm(softmax(zm)))
+    return np.array(npn), np.array(nqn)
+
+
+def _case(T, V, d, scaling, seed):
+    H = random_bf16((T, d), seed)
+    W = random_bf16((V, d), seed + 1, std=2.5 / math.sqrt(d))
+    hq, hs = oracle.quantize_fp8(H, scaling)
+    wq, ws = oracle.quantize_fp8(W, scaling)
+    ids = np.random.default_rng(seed).integers(0, V, size=T).astype(np.int32)
+    return H, W, hq, hs, wq, ws, ids
+
+
+def _gpu(H, W, hq, hs, wq, ws, scaling, ids, tau, **kw):
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    out = acrl.acrl_score_pi_mu(up_bf16(torch, dev, H), up_bf16(torch, dev, W), up(torch, dev, hq),
+                                up(torch, dev, hs), up(torch, dev, wq), up(torch, dev, ws), scaling,
+                                up(torch, dev, ids), inv_temperature=1.0 / tau, divergence=True, **kw)
+    torch.cuda.synchronize()
+    return {k: down(v) for k, v in out.items()}
+
+
+def _check(got, ref, d, norms, rows=None):
+    sel = slice(None) if rows is None else rows
+    delta = 2e-4 * math.sqrt(d / 256.0)
+    np_, nq = norms
+    for k in ("kl_pi_mu", "kl_mu_pi", "l2"):
+        g, r = got[k][sel], ref[k]
+        if k == "l2":
+            tol = 1e-6 + 2 * delta * (np_ + nq)
+        else:
+            tol = 1e-6 + 2 * delta * np.sqrt(2 * np.abs(r))
+        err = np.abs(g - r)
+        assert np.all(err <= tol), "%s: max err %g at %d (got %g, ref %g, tol %g)" % (
+            k, err.max(), err.argmax(), g[err.argmax()], r[err.argmax()], tol[err.argmax()])
+
+
+@pytest.mark.parametrize("T,V,d,scaling,tau", [
+    (300, 1000, 256, oracle.PER_ROW, 1.0), (256, 2048, 256, oracle.PER_TENSOR, 1.0),
+    (513, 300, 128, oracle.MX32, 0.7), (1, 100, 128, oracle.PER_ROW, 1.0),
+    (77, 4128, 384, oracle.PER_TENSOR, 0.7)])
+def test_divergence_matches_oracle(T, V, d, scaling, tau):
+    H, W, hq, hs, wq, ws, ids = _case(T, V, d, scaling, T + V)
+    got = _gpu(H, W, hq, hs, wq, ws, scaling, ids, tau)
+    ref = oracle.divergence(H, W, hq, hs, wq, ws, scaling, inv_temperature=1.0 / tau)
+    _check(got, ref, d, _norms(H, W, hq, hs, wq, ws, scaling, tau, range(T)))
+    assert np.all(got["kl_pi_mu"] > 0) and np.all(got["l2"] > 0)
+
+
+def test_passes_masks_and_slots():
+    T, V, d, sc = 700, 1000, 256, oracle.PER_ROW
+    H, W, hq, hs, wq, ws, ids = _case(T, V, d, sc, 3)
+    one = _gpu(H, W, hq, hs, wq, ws, sc, ids, 1.0)
+    # passes of 256 rows give the same values
+    three = _gpu(H, W, hq, hs, wq, ws, sc, ids, 1.0, div_chunk=256)
+    for k in ("kl_pi_mu", "kl_mu_pi", "l2", "logp_pi", "logp_mu", "entropy_pi"):
+        assert np.array_equal(one[k], three[k]), k
+    # masked rows write 0, rows go to their slots
+    torch, dev = torch_dev()
+    mask = (np.arange(T) % 5 != 2).astype(np.uint8)
+    n_slots = T + 40
+    slots = np.random.default_rng(4).permutation(n_slots)[:T].astype(np.int32)
+    got = _gpu(H, W, hq, hs, wq, ws, sc, ids, 1.0, mask=up(torch, dev, mask), out_slot=up(torch, dev, slots),
+               n_slots=n_slots)
+    for k in ("kl_pi_mu", "kl_mu_pi", "l2"):
+        assert np.array_equal(got[k][slots][mask == 1], one[k][mask == 1]), k
+        assert np.all(got[k][slots][mask == 0] == 0), k
+    # the scoring outputs are those of a call without the measures
+    plain = _gpu_plain(H, W, hq, hs, wq, ws, sc, ids)
+    for k in ("logp_pi", "logp_mu", "entropy_pi", "entropy_mu"):
+        np.testing.assert_allclose(one[k], plain[k], rtol=0, atol=2e-6)
+
+
+def _gpu_plain(H, W, hq, hs, wq, ws, scaling, ids):
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    out = acrl.acrl_score_pi_mu(up_bf16(torch, dev, H), up_bf16(torch, dev, W), up(torch, dev, hq),
+                                up(torch, dev, hs), up(torch, dev, wq), up(torch, dev, ws), scaling,
+                                up(torch, dev, ids))
+    torch.cuda.synchronize()
+    return {k: down(v) for k, v in out.items()}
+
+
+def test_lossless_operands_give_zero():
+    # bf16 and e4m3 hold the operands exactly (scales 1): identical logits,
+    # identical distributions, every measure exactly 0
+    h, w, _ = lossless_integer_case(300, 700, 128, 5)
+    for sc in (oracle.PER_TENSOR, oracle.PER_ROW):
+        hq, hs = oracle.quantize_fp8(h, sc)
+        wq, ws = oracle.quantize_fp8(w, sc)
+        ids = np.zeros(300, np.int32)
+        got = _gpu(h, w, hq, hs, wq, ws, sc, ids, 1e3)
+        for k in ("kl_pi_mu", "kl_mu_pi", "l2"):
+            assert np.all(got[k] == 0), (sc, k)
+
+
+def test_full_size_sampled_rows():
+    """d = 4096, V = 151936 (the q8b head), two passes (16384 + 300 rows):
+    sampled rows against the oracle, every row against Pinsker's bound."""
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    w = inputs.WORKLOADS["q8b"]
+    T = 16384 + 300
+    Hd = inputs.hidden_bf16_torch(w, T, dev)
+    Wd = inputs.weights_bf16_torch(w, dev)
+    hq, hs = acrl.acrl_quantize_fp8(Hd, w.scaling)
+    wq, ws = acrl.acrl_quantize_fp8(Wd, w.scaling)
+    ids = torch.zeros(T, dtype=torch.int32, device=dev)
+    out = acrl.acrl_score_pi_mu(Hd, Wd, hq, hs, wq, ws, w.scaling, ids, divergence=True)
+    torch.cuda.synchronize()
+    got = {k: down(v) for k, v in out.items()}
+    rows = np.array([0, 4097, 16383, 16384, T - 1])
+    idx = torch.from_numpy(rows).to(dev)
+    Hs = down(Hd[idx].view(torch.int16)).view(np.uint16)
+    # the oracle's own quantization of the sampled rows is the GPU's (bit-exact, tested elsewhere);
+    # per-tensor scales come from the whole H, so the oracle takes that scale
+    hq_o, hs_o = oracle.quantize_fp8(down(Hd.view(torch.int16)).view(np.uint16), w.scaling)
+    Wh = down(Wd.view(torch.int16)).view(np.uint16)
+    wq_o, ws_o = oracle.quantize_fp8(Wh, w.scaling)
+    ref = oracle.divergence(Hs, Wh, hq_o[rows], hs_o, wq_o, ws_o, w.scaling)
+    _check(got, ref, w.d, _norms(Hs, Wh, hq_o[rows], hs_o, wq_o, ws_o, w.scaling, 1.0, range(len(rows))), rows)
+    assert np.all(got["kl_pi_mu"] > 0) and np.all(got["kl_mu_pi"] > 0)
+    assert np.all(got["l2"] <= np.sqrt(2 * np.minimum(got["kl_pi_mu"], got["kl_mu_pi"])) * (1 + 1e-3) + 1e-6)
