@@ -43,6 +43,8 @@ def main():
     ap.add_argument("--workload", default="q8b", choices=sorted(inputs.WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="approximate CPU time budget of the oracle baseline (0 = skip)")
+    ap.add_argument("--no-divergence", action="store_true",
+                    help="skip the full-vocabulary KL / Euclidean leg")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the surrogate + LM-head backward leg")
     ap.add_argument("--counters", action="store_true",
@@ -150,6 +152,8 @@ def main():
         torch.cuda.synchronize()
         del src, dst
         step()
+        if not args.no_divergence:
+            divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, 0.0, reps=0)
         if not args.no_backward:
             backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv, 1.0, reps=0)
         torch.cuda.synchronize()
@@ -255,6 +259,8 @@ def main():
     }
 
     line["config"]["hbm_kernels"] = hbm_kernels(torch, acrl, dev, H, w)
+    if not args.no_divergence:
+        line["divergence"] = divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, t_call)
     if not args.no_backward:
         line["backward"] = backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv,
                                         X_ref[0])
@@ -263,6 +269,45 @@ def main():
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, T, H, W, hq, hs, wq, ws, ids, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+
+
+def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, score_ms, reps=2):
+    """The scoring call with the full-vocabulary measures (KL both ways,
+    Euclidean distance) switched on: both score kernels also store their
+    logits (4 B each) for passes of 16384 rows and a streaming kernel reads
+    them back (8 B per vocabulary entry and row)."""
+    V = w.V
+    outs = {}
+
+    def run():
+        return acrl.acrl_score_pi_mu(H, W, hq, hs, wq, ws, w.scaling, ids, inv_temperature=w.inv_temperature,
+                                     out_slot=slots, n_slots=w.slots, outputs=outs, want=("entropy",),
+                                     divergence=True)
+
+    outs.update(run())
+    torch.cuda.synchronize()
+    if reps == 0:  # one untimed pass (counter collection)
+        return None
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        run()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / reps
+    valid = slots.long()
+    kl = outs["kl_pi_mu"][valid]
+    res = {"what": "acrl_score_pi_mu with kl_pi_mu, kl_mu_pi and l2 over the batch's valid tokens",
+           "ms": round(ms, 3), "score_ms_without": round(float(score_ms), 3),
+           "overhead_ms": round(ms - float(score_ms), 3),
+           "logit_bytes_stored_and_read": 2 * 4 * T * V * 2,
+           "mean_kl_pi_mu": float(kl.double().mean().item()),
+           "mean_kl_mu_pi": float(outs["kl_mu_pi"][valid].double().mean().item()),
+           "mean_l2": float(outs["l2"][valid].double().mean().item())}
+    log("divergence:", res)
+    del outs
+    torch.cuda.empty_cache()
+    return res
 
 
 def backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv, X, reps=2):
