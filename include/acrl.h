@@ -333,7 +333,7 @@ acrl_status acrl_controller_step(const acrl_controller_desc* desc, void* stream)
 /* acrl_surrogate -- the ACRL-weighted clipped surrogate and d loss/d logp   */
 /* ======================================================================== *
  * Eq. ACRL (Sec. 4.1) weights the clipped objective of Eq. grpo_objective
- * (Sec. 2.1) token by token with w_t = min(rho_t, C):
+ * (Sec. 2) token by token with w_t = min(rho_t, C):
  *   J = (1/P) sum_g (1/G_g) sum_{i in g} (1/|a_i|) sum_t w_t min(r_t A_t, clip(r_t) A_t),
  *   r_t = exp(logp_new - logp_old), clip(r) = min(max(r, 1 - eps_low), 1 + eps_high),
  * over the valid slots (mask != 0); G_g counts the non-empty responses of

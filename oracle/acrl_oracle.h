@@ -99,7 +99,7 @@ int acrl_ref_score(int64_t n_rows, int64_t d, int64_t V,
 /* ---- Full-vocabulary discrepancy between the two policies --------------- *
  * The paper measures the discrepancy on the sampled token's probabilities
  * (Eq. distance_metric) and names the KL divergence and the Euclidean
- * distance as other measures (remark after Eq. distance_metric; Sec. 6).
+ * distance as other measures (remark after Eq. distance_metric; Sec. 7).
  * Over the whole vocabulary, with p = softmax(z_pi), q = softmax(z_mu):
  *   kl_pi_mu = sum_v p_v (log p_v - log q_v)    (KL(pi || mu))
  *   kl_mu_pi = sum_v q_v (log q_v - log p_v)    (KL(mu || pi))
@@ -180,7 +180,7 @@ int acrl_ref_sample_inverse_cdf(const double* z, int64_t n_rows, int64_t V,
                                 const double* u, int32_t* ids);
 
 /* ---- The ACRL-weighted surrogate and its LM-head backward ------------- *
- * Eq. ACRL (Sec. 4.1), which extends Eq. grpo_objective (Sec. 2.1): the
+ * Eq. ACRL (Sec. 4.1), which extends Eq. grpo_objective (Sec. 2): the
  * objective of a batch is
  *   J = mean over prompts of (1/G) sum_i (1/|a_i|) sum_t w_t min(r_t A_t, clip(r_t) A_t),
  * r_t = pi_theta(a_t) / pi_theta_old(a_t) = exp(logp_new - logp_old),

@@ -240,7 +240,7 @@ __global__ __launch_bounds__(256) void controller_kernel(acrl_controller_desc p)
 
 // ------------------------------------------------------------------ surrogate
 // The ACRL-weighted clipped surrogate (Eq. ACRL on top of the GRPO objective
-// of Sec. 2.1): J = mean over prompts of (1/G) sum_i (1/|a_i|) sum_t
+// of Sec. 2): J = mean over prompts of (1/G) sum_i (1/|a_i|) sum_t
 // w_t min(r_t A_t, clip(r_t) A_t), r_t = exp(logp_new - logp_old); the
 // prompts averaged are those with a non-empty response and G counts a
 // prompt's non-empty responses.  loss = -J, coef_t = d loss / d logp_new_t.
