@@ -51,7 +51,7 @@ enum Epilogue {
 constexpr int kTileV = 256;            // vocabulary rows per workgroup tile
 constexpr int kTileT = 256;            // tokens per workgroup tile
 constexpr int kChunk = 64;             // bytes of K per row per pipeline stage
-constexpr int kThreads = 256;
+constexpr int kThreads = 256;          // 4 waves; score_kernel<..., 8> runs 8 (two per SIMD)
 constexpr int kStageBytes = (kTileV + kTileT) * kChunk;  // 32 KiB
 constexpr int kPackBlock = kTileV * kChunk;               // packed image of one (tile, chunk): 16 KiB
 constexpr float kInitMax = -1.0e30f;   // running max before any logit was seen
@@ -224,18 +224,29 @@ struct Pipe {
   static constexpr int kScaleBytes = (MODE == kMX) ? (kTileV + kTileT) * 4 : 0;  // per stage
   static constexpr int kRowScaleSlots = kStages + 1;
   static constexpr int kRowScaleBytes = (MODE == kFP8Row) ? kRowScaleSlots * kTileV * 4 : 0;
-  static constexpr int kLoadsPerChunk = (MODE == kMX) ? 10 : 8;  // per wave, at least
+  // buffer -> LDS loads per chunk per wave, at least: the two 16 KiB tile
+  // images spread over NW waves (1 KiB per load), plus the MX scales
+  template <int NW>
+  static constexpr int loads_per_chunk() { return 2 * (16 / NW) + (MODE == kMX ? 2 : 0); }
 };
 
-template <int MODE, int EPI>
-__global__ __attribute__((amdgpu_flat_work_group_size(kThreads, kThreads), amdgpu_waves_per_eu(1, 1)))
+// NW = 4: one wave per SIMD, each wave 128 vocabulary rows x 128 tokens
+// (4 x 4 blocks of 32 x 32, 256 accumulators per lane).  NW = 8: two waves
+// per SIMD, each 128 x 64 (4 x 2 blocks, 128 accumulators): while one wave
+// waits at the chunk barrier or runs its softmax epilogue the other keeps
+// the SIMD's matrix core busy.
+template <int MODE, int EPI, int NW>
+__global__ __attribute__((amdgpu_flat_work_group_size(NW * 64, NW * 64), amdgpu_waves_per_eu(NW / 4, NW / 4)))
 void score_kernel(ScoreParams p) {
+  static_assert(NW == 4 || NW == 8, "4 or 8 waves");
+  constexpr int JT = 16 / NW;   // token blocks of 32 per wave
+  constexpr int TW = 32 * JT;   // tokens per wave
   constexpr bool SAMPLE = EPI == kEpiSample;
   constexpr bool SOFTMAX = EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ;
   static_assert(MODE == kBF16 || SOFTMAX, "the backward epilogues take bf16 operands");
   constexpr int NS = Pipe<MODE>::kStages;
   constexpr int SB = Pipe<MODE>::kScaleBytes;
-  constexpr int LPC = Pipe<MODE>::kLoadsPerChunk;
+  constexpr int LPC = Pipe<MODE>::template loads_per_chunk<NW>();
   constexpr int RSB = Pipe<MODE>::kRowScaleBytes;
   __shared__ __attribute__((aligned(1024))) uint8_t lds[NS * (kStageBytes + SB) + RSB];
 
@@ -270,8 +281,8 @@ void score_kernel(ScoreParams p) {
   float bk[4], bz[4];  // sampling: best Gumbel key of the lane and its logit
   int bi[4];           //           and vocabulary row
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    tok[j] = t0 + wt * 128 + j * 32 + r32;
+  for (int j = 0; j < JT; ++j) {
+    tok[j] = t0 + wt * TW + j * 32 + r32;
     const int tc = min(tok[j], p.n_rows - 1);
     id[j] = (EPI == kEpiSample || EPI == kEpiStore) ? -1 : p.ids[tc];
     gl2[j] = 0.0f;
@@ -296,11 +307,11 @@ void score_kernel(ScoreParams p) {
     U[j] = 0.0f;
   }
 
-  f32x16 acc[4][4];
+  f32x16 acc[4][JT];
 #pragma unroll
   for (int b = 0; b < 4; ++b)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
+    for (int j = 0; j < JT; ++j) acc[b][j] = f32x16{};
   if constexpr (EPI == kEpiStore) {
     // one output tile per workgroup: start from C when accumulating
     if (p.c_accumulate) {
@@ -308,7 +319,7 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
       for (int b = 0; b < 4; ++b)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < JT; ++j)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int m = m0 + 32 * b + 8 * (i >> 2) + (i & 3);
@@ -341,17 +352,17 @@ void score_kernel(ScoreParams p) {
     const int v0 = (vt_begin + q) * kTileV;
     const int a_rows = min(kTileV, p.V - v0);  // valid rows of the vocabulary tile
     const __amdgpu_buffer_rsrc_t rsrc_a = make_rsrc(p.a + (int64_t)(vt_begin + q) * tile_bytes, tile_bytes);
-    const uint32_t soff = (uint32_t)kc * kPackBlock + (uint32_t)wave_u * 4096;
-    uint8_t* la = stage_at(stg) + wave_u * 4096;
+    const uint32_t soff = (uint32_t)kc * kPackBlock + (uint32_t)wave_u * (kPackBlock / NW);
+    uint8_t* la = stage_at(stg) + wave_u * (kPackBlock / NW);
     uint8_t* lb = la + kTileV * kChunk;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) buffer_to_lds<16>(rsrc_a, lane_off, soff + k * 1024, la + k * 1024);
+    for (int k = 0; k < 16 / NW; ++k) buffer_to_lds<16>(rsrc_a, lane_off, soff + k * 1024, la + k * 1024);
 #pragma unroll
-    for (int k = 0; k < 4; ++k) buffer_to_lds<16>(rsrc_b, lane_off, soff + k * 1024, lb + k * 1024);
+    for (int k = 0; k < 16 / NW; ++k) buffer_to_lds<16>(rsrc_b, lane_off, soff + k * 1024, lb + k * 1024);
     if constexpr (MODE == kFP8Row) {
       // with a tile's first chunk: its 256 weight-row scales (lane l of wave
       // w moves row 64w + l); they land long before the tile's epilogue
-      if (kc == 0) {
+      if (kc == 0 && (NW == 4 || wave_u < 4)) {  // 64 rows per wave
         const __amdgpu_buffer_rsrc_t rs = make_rsrc(p.a_scale + v0, (uint32_t)a_rows * 4);
         buffer_to_lds<4>(rs, (uint32_t)min(wave_u * 64 + lane, a_rows - 1) * 4, 0,
                          reinterpret_cast<uint8_t*>(rowscales_at(q)) + wave_u * 64 * 4);
@@ -367,9 +378,9 @@ void score_kernel(ScoreParams p) {
       const __amdgpu_buffer_rsrc_t sa = make_rsrc(p.a_mx + (int64_t)v0 * p.mx_row_bytes, (uint32_t)a_rows * mrb);
       const __amdgpu_buffer_rsrc_t sb = make_rsrc(p.b_mx + (int64_t)t0 * p.mx_row_bytes, (uint32_t)b_rows * mrb);
       const uint32_t soff = (uint32_t)(kc >> 1) * 4;
-      buffer_to_lds<4>(sa, (uint32_t)min(wave_u * 64 + lane, a_rows - 1) * mrb, soff,
+      if (NW == 4 || wave_u < 4) buffer_to_lds<4>(sa, (uint32_t)min(wave_u * 64 + lane, a_rows - 1) * mrb, soff,
                        scales_at(stg) + wave_u * 64 * 4);
-      buffer_to_lds<4>(sb, (uint32_t)min(wave_u * 64 + lane, b_rows - 1) * mrb, soff,
+      if (NW == 4 || wave_u < 4) buffer_to_lds<4>(sb, (uint32_t)min(wave_u * 64 + lane, b_rows - 1) * mrb, soff,
                        scales_at(stg) + (kTileV + wave_u * 64) * 4);
     }
   };
@@ -408,10 +419,10 @@ void score_kernel(ScoreParams p) {
     if constexpr (MODE == kBF16) return read16x2(row + frag_off(grp));
     else return read16x2(row);
   };
-  auto read_b = [&](int stg, int grp, FragT (&bf)[4]) {
+  auto read_b = [&](int stg, int grp, FragT (&bf)[JT]) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const uint8_t* row = stage_at(stg) + (kTileV + wt * 128 + j * 32 + r32) * kChunk;
+    for (int j = 0; j < JT; ++j) {
+      const uint8_t* row = stage_at(stg) + (kTileV + wt * TW + j * 32 + r32) * kChunk;
       if constexpr (MODE == kBF16) bf[j] = read16x2(row + frag_off(grp));
       else bf[j] = read16x2(row);
     }
@@ -423,14 +434,14 @@ void score_kernel(ScoreParams p) {
   auto read_sa = [&](int stg, int grp) -> int {
     return scales_at(stg)[(wv * 128 + (grp & 3) * 32 + r32) * 4 + (stg & 1) * 2 + g];
   };
-  auto read_sb = [&](int stg, int (&sb)[4]) {
+  auto read_sb = [&](int stg, int (&sb)[JT]) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) sb[j] = scales_at(stg)[(kTileV + wt * 128 + j * 32 + r32) * 4 + (stg & 1) * 2 + g];
+    for (int j = 0; j < JT; ++j) sb[j] = scales_at(stg)[(kTileV + wt * TW + j * 32 + r32) * 4 + (stg & 1) * 2 + g];
   };
-  auto mfma_group = [&](int grp, const FragT& fa, const FragT (&fb)[4], int sa, const int (&sb)[4]) {
+  auto mfma_group = [&](int grp, const FragT& fa, const FragT (&fb)[JT], int sa, const int (&sb)[JT]) {
     const int bb = grp & 3;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < JT; ++j) {
       if constexpr (MODE == kBF16) {
         acc[bb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb[j], acc[bb][j], 0, 0, 0);
       } else if constexpr (MODE == kMX) {
@@ -488,7 +499,7 @@ void score_kernel(ScoreParams p) {
           }
         }
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < JT; ++j) {
           float v[16];
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
@@ -498,7 +509,7 @@ void score_kernel(ScoreParams p) {
           if constexpr (EPI == kEpiSoftmaxZ) {
             // the logits z = acc * scale (natural units) of the lane's token
             // row: 4 runs of 4 consecutive vocabulary entries (16 bytes each)
-            float* zr = p.zbuf + (int64_t)(tt * kTileT + wt * 128 + j * 32 + r32) * p.z_ld + v0 + 32 * b + 4 * g;
+            float* zr = p.zbuf + (int64_t)(tt * kTileT + wt * TW + j * 32 + r32) * p.z_ld + v0 + 32 * b + 4 * g;
 #pragma unroll
             for (int qq = 0; qq < 4; ++qq)
               *reinterpret_cast<f32x4*>(zr + 8 * qq) =
@@ -607,7 +618,7 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
+      for (int j = 0; j < JT; ++j) {
         float dz[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
@@ -619,7 +630,7 @@ void score_kernel(ScoreParams p) {
         // rows = tokens: the lane's token row, 4 consecutive vocabulary
         // values (8 bytes) per 16-byte column q
         {
-          const int rr = wt * 128 + 32 * j + r32;
+          const int rr = wt * TW + 32 * j + r32;
           const int kc = tile * 8 + wv * 4 + b;
           uint8_t* row = p.gz_t + (((int64_t)tt * p.kch_v + kc) * kTileT + rr) * kChunk + 8 * g;
 #pragma unroll
@@ -632,7 +643,7 @@ void score_kernel(ScoreParams p) {
         // after one exchange the even lane stores the pair of row i, the odd
         // lane the pair of row i+1 (4 bytes each)
         {
-          const int kc = tt * 8 + wt * 4 + j;
+          const int kc = tt * 8 + wt * JT + j;
           uint8_t* img = p.gz_v + ((int64_t)tile * p.kch_t + kc) * kTileV * kChunk;
 #pragma unroll
           for (int i = 0; i < 16; i += 2) {
@@ -658,7 +669,7 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < JT; ++j)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int m = m0 + 32 * b + 8 * (i >> 2) + (i & 3);
@@ -700,8 +711,8 @@ void score_kernel(ScoreParams p) {
   // has an even number of chunks), so the next chunk's fragments are read
   // straight into the registers it will use.
   struct Frags {
-    FragT a[L], b[4];
-    int sa[L], sb[4];
+    FragT a[L], b[JT];
+    int sa[L], sb[JT];
   };
   Frags f0, f1;
 #pragma unroll
@@ -712,7 +723,7 @@ void score_kernel(ScoreParams p) {
   }
   read_b(0, 0, f0.b);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) f0.sb[j] = 0;
+  for (int j = 0; j < JT; ++j) f0.sb[j] = 0;
   if constexpr (MODE == kMX) read_sb(0, f0.sb);
 
   // LDS read instructions issued in group k (for group k + L)
@@ -720,7 +731,7 @@ void score_kernel(ScoreParams p) {
     const int t = k + L, tt = t % G;
     constexpr int per_frag = (MODE == kBF16) ? 1 : 2;
     int n = per_frag + (MODE == kMX ? 1 : 0);                               // A (+ its MX scale)
-    if (tt % 4 == 0) n += 4 * per_frag + (MODE == kMX && tt == 0 ? 4 : 0);  // B of a new step
+    if (tt % 4 == 0) n += JT * per_frag + (MODE == kMX && tt == 0 ? JT : 0);  // B of a new step
     return n;
   };
   int stg = 0;  // stage of the current chunk
@@ -729,7 +740,7 @@ void score_kernel(ScoreParams p) {
     const bool has_next = kSteady || it + 1 < n_iter;
     const int nst = stg + 1 == NS ? 0 : stg + 1;
     FragT af[G];       // A of this chunk's groups
-    FragT bf[2][4];    // B of this chunk's K steps (BF16: 2, FP8: 1)
+    FragT bf[2][JT];    // B of this chunk's K steps (BF16: 2, FP8: 1)
     int sa[G];
 #pragma unroll
     for (int l = 0; l < L; ++l) {
@@ -737,7 +748,7 @@ void score_kernel(ScoreParams p) {
       sa[l] = cur.sa[l];
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) bf[0][j] = cur.b[j];
+    for (int j = 0; j < JT; ++j) bf[0][j] = cur.b[j];
 #pragma unroll
     for (int k = 0; k < G; ++k) {
       const int t = k + L;  // group whose fragments are read now
@@ -769,7 +780,7 @@ void score_kernel(ScoreParams p) {
         // keep this group's LDS reads ahead of its MFMAs (the scheduler
         // would otherwise sink each read to just before its use)
         sched_ds_reads(reads_at(k));
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // 4 MFMAs
+        __builtin_amdgcn_sched_group_barrier(0x008, JT, 0);  // JT MFMAs
       }
     }
     stg = nst;
@@ -795,7 +806,7 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[b][j] = f32x16{};
+      for (int j = 0; j < JT; ++j) acc[b][j] = f32x16{};
   }
   if constexpr (!SOFTMAX) return;
   __syncthreads();  // every wave is done with the stages before LDS is reused
@@ -810,7 +821,7 @@ void score_kernel(ScoreParams p) {
     }
   };
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < JT; ++j) {
     const float M2 = __shfl_xor(M[j], 32), S2 = __shfl_xor(S[j], 32), U2 = __shfl_xor(U[j], 32);
     merge_state(M[j], S[j], U[j], M2, S2, U2);
     if constexpr (SAMPLE) {
@@ -823,8 +834,8 @@ void score_kernel(ScoreParams p) {
   float* xch = reinterpret_cast<float*>(lds);  // LDS is free after the last barrier
   if (wv == 1 && g == 0) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int k = wt * 128 + j * 32 + r32;
+    for (int j = 0; j < JT; ++j) {
+      const int k = wt * TW + j * 32 + r32;
       xch[XS * k + 0] = M[j];
       xch[XS * k + 1] = S[j];
       xch[XS * k + 2] = U[j];
@@ -839,8 +850,8 @@ void score_kernel(ScoreParams p) {
   if (wv == 0 && g == 0) {
     const int64_t plane = (int64_t)p.n_strips * p.n_rows;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int k = wt * 128 + j * 32 + r32;
+    for (int j = 0; j < JT; ++j) {
+      const int k = wt * TW + j * 32 + r32;
       merge_state(M[j], S[j], U[j], xch[XS * k + 0], xch[XS * k + 1], xch[XS * k + 2]);
       if constexpr (SAMPLE)
         take_best(bk[j], bz[j], bi[j], xch[XS * k + 3], xch[XS * k + 4], __float_as_int(xch[XS * k + 5]));
@@ -858,6 +869,20 @@ void score_kernel(ScoreParams p) {
       }
     }
   }
+}
+
+// Waves per workgroup of each instantiation (measured on the MI355X): two
+// per SIMD where the variant fits its registers without spilling and runs
+// faster; one per SIMD otherwise.
+template <int MODE, int EPI>
+constexpr int waves_for() {
+  return ((EPI == kEpiSoftmax || EPI == kEpiSoftmaxZ) && (MODE == kBF16 || MODE == kFP8Tensor)) ? 8 : 4;
+}
+
+template <int MODE, int EPI>
+void launch_score_kernel(unsigned grid, const ScoreParams& p, hipStream_t s) {
+  constexpr int NW = waves_for<MODE, EPI>();
+  hipLaunchKernelGGL((score_kernel<MODE, EPI, NW>), dim3(grid), dim3(NW * 64), 0, s, p);
 }
 
 // Packed operand image read by score_kernel: for each 256-row tile and each
@@ -1222,16 +1247,16 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   auto launch_mu = [&](const ScoreParams& q, unsigned g, auto epi_tag) {
     constexpr int E = decltype(epi_tag)::value;
     if (dsc.mu_scaling == ACRL_SCALE_MX32)
-      hipLaunchKernelGGL((score_kernel<kMX, E>), dim3(g), dim3(kThreads), 0, s, q);
+      launch_score_kernel<kMX, E>(g, q, s);
     else if (dsc.mu_scaling == ACRL_SCALE_PER_ROW)
-      hipLaunchKernelGGL((score_kernel<kFP8Row, E>), dim3(g), dim3(kThreads), 0, s, q);
+      launch_score_kernel<kFP8Row, E>(g, q, s);
     else
-      hipLaunchKernelGGL((score_kernel<kFP8Tensor, E>), dim3(g), dim3(kThreads), 0, s, q);
+      launch_score_kernel<kFP8Tensor, E>(g, q, s);
   };
   const bool div = dsc.kl_pi_mu || dsc.kl_mu_pi || dsc.l2;
   trace(0, s);
   if (!div) {
-    hipLaunchKernelGGL((score_kernel<kBF16, kEpiSoftmax>), dim3(grid), dim3(kThreads), 0, s, pp);
+    launch_score_kernel<kBF16, kEpiSoftmax>(grid, pp, s);
     trace(1, s);
     launch_mu(pm, grid, std::integral_constant<int, kEpiSoftmax>{});
   } else {
@@ -1250,7 +1275,7 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
       pz.n_tblocks = ntb;
       pz.zbuf = zbuf[0];
       pz.z_ld = z_ld;
-      hipLaunchKernelGGL((score_kernel<kBF16, kEpiSoftmaxZ>), dim3(g), dim3(kThreads), 0, s, pz);
+      launch_score_kernel<kBF16, kEpiSoftmaxZ>(g, pz, s);
       ScoreParams pq = pm;
       pq.tt_offset = tt0;
       pq.n_ttiles = nt;
@@ -1405,7 +1430,7 @@ hipError_t launch_backward(const acrl_backward_desc& dsc, const BackwardPlan& pl
       pg.gz_v = img_zv;
       pg.kch_v = pl.kch_v;
       pg.kch_t = kch_t;
-      hipLaunchKernelGGL((score_kernel<kBF16, kEpiGrad>), dim3((unsigned)sp.grid), dim3(kThreads), 0, s, pg);
+      launch_score_kernel<kBF16, kEpiGrad>((unsigned)sp.grid, pg, s);
     }
     // dH[chunk] = dZ W: A = dZ (rows = tokens), B = W^T (rows = d), K = vocabulary
     if (dh) {
@@ -1421,7 +1446,7 @@ hipError_t launch_backward(const acrl_backward_desc& dsc, const BackwardPlan& pl
       pc.ldc = d;
       pc.c_rows = (int)rows;
       pc.c_accumulate = 0;
-      hipLaunchKernelGGL((score_kernel<kBF16, kEpiStore>), dim3(grid), dim3(kThreads), 0, s, pc);
+      launch_score_kernel<kBF16, kEpiStore>(grid, pc, s);
     }
     // dW (+)= dZ^T H: A = dZ^T (rows = vocabulary), B = H^T (rows = d), K = tokens
     if (dw) {
@@ -1437,7 +1462,7 @@ hipError_t launch_backward(const acrl_backward_desc& dsc, const BackwardPlan& pl
       pc.ldc = d;
       pc.c_rows = (int)V;
       pc.c_accumulate = (r0 > 0 || dsc.accumulate_dw) ? 1 : 0;
-      hipLaunchKernelGGL((score_kernel<kBF16, kEpiStore>), dim3(grid), dim3(kThreads), 0, s, pc);
+      launch_score_kernel<kBF16, kEpiStore>(grid, pc, s);
     }
   }
   return hipGetLastError();
@@ -1480,14 +1505,14 @@ hipError_t launch_sample(const acrl_sample_desc& dsc, const ScorePlan& pl, hipSt
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
     pm.a_mx = static_cast<const uint8_t*>(dsc.wq_scales);
     pm.b_mx = static_cast<const uint8_t*>(dsc.hq_scales);
-    hipLaunchKernelGGL((score_kernel<kMX, kEpiSample>), dim3(grid), dim3(kThreads), 0, s, pm);
+    launch_score_kernel<kMX, kEpiSample>(grid, pm, s);
   } else {
     pm.a_scale = static_cast<const float*>(dsc.wq_scales);
     pm.b_scale = static_cast<const float*>(dsc.hq_scales);
     if (dsc.mu_scaling == ACRL_SCALE_PER_ROW)
-      hipLaunchKernelGGL((score_kernel<kFP8Row, kEpiSample>), dim3(grid), dim3(kThreads), 0, s, pm);
+      launch_score_kernel<kFP8Row, kEpiSample>(grid, pm, s);
     else
-      hipLaunchKernelGGL((score_kernel<kFP8Tensor, kEpiSample>), dim3(grid), dim3(kThreads), 0, s, pm);
+      launch_score_kernel<kFP8Tensor, kEpiSample>(grid, pm, s);
   }
   SampleMergeParams mp{};
   mp.n_rows = (int)dsc.n_rows;
