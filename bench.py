@@ -219,10 +219,18 @@ def main():
     # HBM traffic of each score kernel from the committed counter summary, if current
     tr = profiling.load_traffic(os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
                                              "score_%s_traffic.md" % w.name))
-    mu_kernel = "score_kernel<%d, false>" % {inputs.PER_TENSOR: 1, inputs.PER_ROW: 2, inputs.MX32: 3}[w.scaling]
-    for roof, kname in ((roof_pi, "score_kernel<0, false>"), (roof_mu, mu_kernel)):
-        if tr is not None and kname in tr["kernels"]:
-            roof["traffic"] = round(tr["kernels"][kname]["traffic_bytes"])
+    mu_mode = {inputs.PER_TENSOR: 1, inputs.PER_ROW: 2, inputs.MX32: 3}[w.scaling]
+
+    def scorer_row(mode):  # the scoring instantiation <mode, softmax epilogue, any wave count>
+        if tr is None:
+            return None
+        keys = [k for k in tr["kernels"] if k.startswith("score_kernel<%d, 0" % mode)]
+        return tr["kernels"][keys[0]] if keys else None
+
+    for roof, mode in ((roof_pi, 0), (roof_mu, mu_mode)):
+        row = scorer_row(mode)
+        if row is not None:
+            roof["traffic"] = round(row["traffic_bytes"])
             roof["traffic_unit"] = "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     # fraction of the combined MFMA roofline: ideal time at both peaks / measured step time
     ideal_ms = (flops / (PEAK_TFLOPS["bf16"] * 1e12) + flops / (PEAK_TFLOPS["fp8"] * 1e12)) * 1e3

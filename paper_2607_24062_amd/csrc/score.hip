@@ -876,7 +876,9 @@ void score_kernel(ScoreParams p) {
 // faster; one per SIMD otherwise.
 template <int MODE, int EPI>
 constexpr int waves_for() {
-  return ((EPI == kEpiSoftmax || EPI == kEpiSoftmaxZ) && (MODE == kBF16 || MODE == kFP8Tensor)) ? 8 : 4;
+  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor)) || (EPI == kEpiSoftmaxZ && MODE == kBF16))
+             ? 8
+             : 4;
 }
 
 template <int MODE, int EPI>
