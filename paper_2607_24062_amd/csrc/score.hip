@@ -529,30 +529,44 @@ void score_kernel(ScoreParams p) {
           S[j] *= al;
           M[j] = Mn;
           const float nM = -Mn;
-          float t[16], e[16];
+          // exponentials and sums in two halves of H = 8 values (fewer live
+          // registers than all 16 at once).  Every variant sums in this same
+          // order, so pi and mu give bitwise equal statistics on equal logits.
+          constexpr int H = 8;
+          float sh[16 / H], uh[16 / H];
 #pragma unroll
-          for (int i = 0; i < 16; ++i) t[i] = fmaf(v[i], c2[j], nM);
+          for (int h0 = 0; h0 < 16; h0 += H) {
+            float t[H], e[H];
 #pragma unroll
-          for (int i = 0; i < 16; ++i) e[i] = fast_exp2(t[i]);
-          if constexpr (kTail) {
+            for (int i = 0; i < H; ++i) t[i] = fmaf(v[h0 + i], c2[j], nM);
 #pragma unroll
-            for (int i = 0; i < 16; ++i) e[i] *= fminf(fmaxf(nv - (float)(16 * b + i), 0.0f), 1.0f);
-          }
-          float s8[8], u8[8];
+            for (int i = 0; i < H; ++i) e[i] = fast_exp2(t[i]);
+            if constexpr (kTail) {
 #pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            s8[i] = e[2 * i] + e[2 * i + 1];
-            u8[i] = fmaf(e[2 * i + 1], t[2 * i + 1], e[2 * i] * t[2 * i]);
-          }
-#pragma unroll
-          for (int w = 4; w >= 1; w >>= 1)
-#pragma unroll
-            for (int i = 0; i < w; ++i) {
-              s8[i] += s8[i + w];
-              u8[i] += u8[i + w];
+              for (int i = 0; i < H; ++i) e[i] *= fminf(fmaxf(nv - (float)(16 * b + h0 + i), 0.0f), 1.0f);
             }
-          S[j] += s8[0];
-          U[j] += u8[0];
+            float s8[H / 2], u8[H / 2];
+#pragma unroll
+            for (int i = 0; i < H / 2; ++i) {
+              s8[i] = e[2 * i] + e[2 * i + 1];
+              u8[i] = fmaf(e[2 * i + 1], t[2 * i + 1], e[2 * i] * t[2 * i]);
+            }
+#pragma unroll
+            for (int w = H / 4; w >= 1; w >>= 1)
+#pragma unroll
+              for (int i = 0; i < w; ++i) {
+                s8[i] += s8[i + w];
+                u8[i] += u8[i + w];
+              }
+            sh[h0 / H] = s8[0];
+            uh[h0 / H] = u8[0];
+          }
+          if constexpr (H == 8) {
+            sh[0] += sh[1];
+            uh[0] += uh[1];
+          }
+          S[j] += sh[0];
+          U[j] += uh[0];
           // finish the update here, ahead of the branch below: otherwise the
           // pass is sunk past it and the values of all 16 blocks stay live
           asm volatile("" : "+v"(M[j]), "+v"(S[j]), "+v"(U[j]));
