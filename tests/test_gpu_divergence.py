@@ -74,7 +74,8 @@ def _check(got, ref, d, norms, rows=None):
 @pytest.mark.parametrize("T,V,d,scaling,tau", [
     (300, 1000, 256, oracle.PER_ROW, 1.0), (256, 2048, 256, oracle.PER_TENSOR, 1.0),
     (513, 300, 128, oracle.MX32, 0.7), (1, 100, 128, oracle.PER_ROW, 1.0),
-    (77, 4128, 384, oracle.PER_TENSOR, 0.7)])
+    (77, 4128, 384, oracle.PER_TENSOR, 0.7), (130, 1001, 256, oracle.PER_ROW, 1.0),
+    (40, 257, 128, oracle.MX32, 1.0)])
 def test_divergence_matches_oracle(T, V, d, scaling, tau):
     H, W, hq, hs, wq, ws, ids = _case(T, V, d, scaling, T + V)
     got = _gpu(H, W, hq, hs, wq, ws, scaling, ids, tau)
