@@ -152,13 +152,7 @@ def test_small_workload_end_to_end():
     red = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, sc["logp_pi"], sc["logp_mu"], m, g,
                                        entropy_pi=sc["entropy_pi"], entropy_mu=sc["entropy_mu"])
     torch.cuda.synchronize()
-    X = float(down(red["stats"])[0]) * 0.5
-    alpha, weight = acrl.acrl_controller_step(w.B, w.L, w.n_prompts, m, g, sc["logp_pi"], sc["logp_mu"],
-                                              up(torch, dev, c["adv"]), False, acrl.Y_GROUP,
-                                              red["seq_mean_d"], red["group_y"], red["stats"],
-                                              X, 0.65, 3.0)
-    torch.cuda.synchronize()
-    # oracle chain
+    # oracle chain (its own quantization, scores and reduce)
     sref = oracle.score(c["H"], c["W"], c["hq"], c["hs"], c["wq"], c["ws"], w.scaling, c["ids"],
                         inv_temperature=w.inv_temperature)
     lp_pi = np.zeros(w.slots)
@@ -166,6 +160,13 @@ def test_small_workload_end_to_end():
     lp_pi[c["slots"]] = sref["logp_pi"]
     lp_mu[c["slots"]] = sref["logp_mu"]
     rref = oracle.discrepancy_reduce(w.B, w.L, lp_pi, lp_mu, c["mask"], c["groups"], w.n_prompts)
+    # the threshold X is taken from the oracle chain and handed to both sides
+    X = float(rref["stats"][0]) * 0.5
+    alpha, weight = acrl.acrl_controller_step(w.B, w.L, w.n_prompts, m, g, sc["logp_pi"], sc["logp_mu"],
+                                              up(torch, dev, c["adv"]), False, acrl.Y_GROUP,
+                                              red["seq_mean_d"], red["group_y"], red["stats"],
+                                              X, 0.65, 3.0)
+    torch.cuda.synchronize()
     gl = down(sc["logp_pi"])
     assert np.abs(gl - lp_pi).max() <= TOL_LOGP
     assert np.abs(down(sc["logp_mu"]) - lp_mu).max() <= TOL_LOGP

@@ -42,8 +42,12 @@ def test_sample_matches_oracle(scaling, T, V, d, inv_temp):
     torch.cuda.synchronize()
     ids, lp = down(ids), down(lp)
     assert ((ids >= 0) & (ids < V)).all()
-    z = np.stack([oracle.logits_mu(down(hq)[r], oracle._row_scale(down(hs), scaling, r), down(wq),
-                                   down(ws), scaling, inv_temp) for r in range(T)])
+    # the oracle's own quantization (bit-exact with the device's, checked here too)
+    hq_o, hs_o = oracle.quantize_fp8(H, scaling)
+    wq_o, ws_o = oracle.quantize_fp8(W, scaling)
+    assert np.array_equal(down(hq), hq_o) and np.array_equal(down(wq), wq_o)
+    z = np.stack([oracle.logits_mu(hq_o[r], oracle._row_scale(hs_o, scaling, r), wq_o, ws_o, scaling, inv_temp)
+                  for r in range(T)])
     keys = _oracle_keys(z, seed, off)
     best = keys.max(axis=1)
     srt = np.sort(keys, axis=1)
@@ -77,8 +81,9 @@ def test_sample_chunked_equals_one_shot_and_frequencies():
     torch.cuda.synchronize()
     a, b = down(a), down(b)
     assert np.array_equal(a, b)
-    z = oracle.logits_mu(down(hq)[0], oracle._row_scale(down(hs), oracle.PER_ROW, 0), down(wq), down(ws),
-                         oracle.PER_ROW, 1.0)
+    hq_o, hs_o = oracle.quantize_fp8(H[:1], oracle.PER_ROW)
+    wq_o, ws_o = oracle.quantize_fp8(W, oracle.PER_ROW)
+    z = oracle.logits_mu(hq_o[0], oracle._row_scale(hs_o, oracle.PER_ROW, 0), wq_o, ws_o, oracle.PER_ROW, 1.0)
     p = np.exp(z - z.max())
     p /= p.sum()
     freq = np.bincount(a, minlength=V) / T

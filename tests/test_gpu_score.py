@@ -41,6 +41,19 @@ def _gpu_score(H, W, ids, scaling, inv_temp=1.0, mask=None, out_slot=None, n_slo
     return res, q
 
 
+def _oracle_score(H, W, scaling, ids, q=None, rounding=oracle.ROUND_NEAREST_EVEN, **kw):
+    """The oracle's own chain on the same bf16 inputs: its quantization of H
+    and W, then its scores.  The GPU's codes and scales q, if given, must equal
+    the oracle's bit for bit (they never feed the oracle)."""
+    hq, hs = oracle.quantize_fp8(H, scaling, rounding=rounding)
+    wq, ws = oracle.quantize_fp8(W, scaling, rounding=rounding)
+    if q is not None:
+        assert np.array_equal(q["hq"], hq) and np.array_equal(q["wq"], wq)
+        assert np.array_equal(q["hs"].view(np.uint8), hs.view(np.uint8))
+        assert np.array_equal(q["ws"].view(np.uint8), ws.view(np.uint8))
+    return oracle.score(H, W, hq, hs, wq, ws, scaling, ids, **kw)
+
+
 def _compare(res, ref, V, rows=None, slots=None, exact_logit=False):
     rows = np.arange(len(ref["logp_pi"])) if rows is None else rows
     slots = rows if slots is None else slots
@@ -86,7 +99,7 @@ def test_ragged_shapes(scaling, T, V, d):
     ids = r.integers(0, V, size=T).astype(np.int32)
     ids[: min(T, 6)] = [0, V - 1, min(127, V - 1), min(128, V - 1), min(255, V - 1), min(256, V - 1)][: min(T, 6)]
     res, q = _gpu_score(H, W, ids, scaling, 1.0)
-    ref = oracle.score(H, W, q["hq"], q["hs"], q["wq"], q["ws"], scaling, ids)
+    ref = _oracle_score(H, W, scaling, ids, q)
     _compare(res, ref, V)
 
 
@@ -104,7 +117,7 @@ def test_exact_integer_logits(scaling):
     assert np.array_equal(res["logit_mu"].astype(np.float64), want)
     assert np.array_equal(res["logp_pi"], res["logp_mu"])
     assert np.array_equal(res["entropy_pi"], res["entropy_mu"])
-    ref = oracle.score(H, W, q["hq"], q["hs"], q["wq"], q["ws"], scaling, ids)
+    ref = _oracle_score(H, W, scaling, ids, q)
     _compare(res, ref, V, exact_logit=True)
 
 
@@ -115,8 +128,7 @@ def test_temperature_and_mask():
     ids = np.random.default_rng(7).integers(0, V, size=T).astype(np.int32)
     mask = (np.random.default_rng(8).random(T) < 0.7).astype(np.uint8)
     res, q = _gpu_score(H, W, ids, oracle.PER_ROW, inv_temp=1 / 0.7, mask=mask)
-    ref = oracle.score(H, W, q["hq"], q["hs"], q["wq"], q["ws"], oracle.PER_ROW, ids, mask,
-                       inv_temperature=1 / 0.7)
+    ref = _oracle_score(H, W, oracle.PER_ROW, ids, q, mask=mask, inv_temperature=1 / 0.7)
     on = np.flatnonzero(mask)
     _compare(res, ref, V, rows=on)
     off = np.flatnonzero(mask == 0)
@@ -134,8 +146,7 @@ def test_invalid_ids_flag_and_nan():
     assert res["error_flag"] != 0
     assert np.isnan(res["logp_pi"][[3, 7]]).all() and np.isnan(res["logp_mu"][[3, 7]]).all()
     good = np.setdiff1d(np.arange(T), [3, 7])
-    ref = oracle.score(H, W, q["hq"], q["hs"], q["wq"], q["ws"], oracle.PER_ROW,
-                       np.where((ids >= 0) & (ids < V), ids, 0).astype(np.int32))
+    ref = _oracle_score(H, W, oracle.PER_ROW, np.where((ids >= 0) & (ids < V), ids, 0).astype(np.int32), q)
     _compare(res, ref, V, rows=good)
 
 
@@ -187,16 +198,16 @@ def test_full_size_sampled_rows(name):
     torch.cuda.synchronize()
     idx = torch.from_numpy(rows).to(dev)
     Hs = h.index_select(0, idx).cpu().view(torch.int16).numpy().view(np.uint16)
-    hqs = down(hq.index_select(0, idx))
-    if w.scaling == oracle.PER_ROW:
-        hss = down(hs)[rows]
-    elif w.scaling == oracle.MX32:
-        hss = down(hs)[rows]
-    else:
-        hss = down(hs)
     Wb = W.cpu().view(torch.int16).numpy().view(np.uint16)
-    ref = oracle.score(Hs, Wb, hqs, hss, down(wq), down(ws), w.scaling, ids_np[rows],
-                       inv_temperature=w.inv_temperature)
+    # the oracle quantizes on its own: per-row / MX scales belong to each row,
+    # the per-tensor scale to the whole of H
+    wq_o, ws_o = oracle.quantize_fp8(Wb, w.scaling)
+    if w.scaling == oracle.PER_TENSOR:
+        hq_all, hs_o = oracle.quantize_fp8(h.cpu().view(torch.int16).numpy().view(np.uint16), w.scaling)
+        hq_o = hq_all[rows]
+    else:
+        hq_o, hs_o = oracle.quantize_fp8(Hs, w.scaling)
+    ref = oracle.score(Hs, Wb, hq_o, hs_o, wq_o, ws_o, w.scaling, ids_np[rows], inv_temperature=w.inv_temperature)
     res = {k: down(v)[rows] for k, v in out.items()}
     _compare(res, ref, w.V)
     # every row's outputs are finite and in range
@@ -240,26 +251,37 @@ def test_long_workload_chunked():
     idx = torch.from_numpy(rows).to(dev)
     Hs = h.index_select(0, idx).cpu().view(torch.int16).numpy().view(np.uint16)
     Wb = W.cpu().view(torch.int16).numpy().view(np.uint16)
-    ref = oracle.score(Hs, Wb, down(hq.index_select(0, idx)), down(hs)[rows], down(wq), down(ws),
-                       w.scaling, ids_np[rows], inv_temperature=w.inv_temperature)
+    hq_o, hs_o = oracle.quantize_fp8(Hs, w.scaling)   # per-row scales: each row's own
+    wq_o, ws_o = oracle.quantize_fp8(Wb, w.scaling)
+    ref = oracle.score(Hs, Wb, hq_o, hs_o, wq_o, ws_o, w.scaling, ids_np[rows], inv_temperature=w.inv_temperature)
     for tag in ("pi", "mu"):
         got = down(outs["logp_" + tag])[slots[rows]]
         assert np.abs(got - ref["logp_" + tag]).max() <= TOL_LOGP
-    # ragged segmented reduce over the whole slot array
+    # ragged segmented reduce over the whole slot array of the scored batch:
+    # its per-sequence sums are the fp64 sums of the per-token log-ratios it
+    # was given (a property at any size), the lengths are the workload's
     mask = inputs.mask(w).reshape(-1)
     groups = inputs.group_of_seq(w)
     red = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, outs["logp_pi"], outs["logp_mu"],
                                        up(torch, dev, mask), up(torch, dev, groups),
                                        entropy_pi=outs["entropy_pi"], entropy_mu=outs["entropy_mu"])
     torch.cuda.synchronize()
-    lp_pi, lp_mu = down(outs["logp_pi"]), down(outs["logp_mu"])
-    oref = oracle.discrepancy_reduce(w.B, w.L, lp_pi, lp_mu, mask, groups, w.n_prompts,
-                                     ent_pi=down(outs["entropy_pi"]), ent_mu=down(outs["entropy_mu"]))
-    assert np.array_equal(down(red["seq_len"]), oref["seq_len"])
-    n = oref["seq_len"].astype(np.float64)
-    assert (np.abs(down(red["seq_sum_logratio"]) - oref["seq_sum_logratio"]) <= 1e-9 * np.maximum(n, 1)).all()
-    np.testing.assert_allclose(down(red["group_y"]), oref["group_y"], rtol=1e-5, atol=1e-12)
-    assert abs(down(red["stats"])[0] - oref["stats"][0]) <= 1e-5 * abs(oref["stats"][0]) + 1e-12
+    assert np.array_equal(down(red["seq_len"]), inputs.lengths(w))
+    lr = (down(outs["logp_pi"]).astype(np.float64) - down(outs["logp_mu"]).astype(np.float64)).reshape(w.B, w.L)
+    sums = np.array([np.sum(lr[i, :n]) for i, n in enumerate(inputs.lengths(w))])
+    np.testing.assert_allclose(down(red["seq_sum_logratio"]), sums, rtol=1e-9, atol=1e-9)
+    # and the reduce against the oracle's on seeded log-probs of this ragged shape
+    r = np.random.default_rng(w.seed)
+    lp_pi = np.log(r.uniform(1e-6, 1, size=w.slots)).astype(np.float32)
+    lp_mu = (lp_pi + r.normal(0, 0.1, size=w.slots)).astype(np.float32)
+    red2 = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, up(torch, dev, lp_pi), up(torch, dev, lp_mu),
+                                        up(torch, dev, mask), up(torch, dev, groups))
+    torch.cuda.synchronize()
+    oref = oracle.discrepancy_reduce(w.B, w.L, lp_pi, lp_mu, mask, groups, w.n_prompts)
+    assert np.array_equal(down(red2["seq_len"]), oref["seq_len"])
+    np.testing.assert_allclose(down(red2["seq_sum_logratio"]), oref["seq_sum_logratio"], rtol=1e-12, atol=1e-9)
+    np.testing.assert_allclose(down(red2["group_y"]), oref["group_y"], rtol=1e-6, atol=1e-12)
+    np.testing.assert_allclose(down(red2["stats"]), oref["stats"], rtol=1e-10, atol=1e-15)
     del h, W, hq, wq, outs
     torch.cuda.empty_cache()
 
@@ -279,6 +301,7 @@ def test_truncated_fp8_end_to_end(scaling):
     hq_o, hs_o = oracle.quantize_fp8(H, scaling, rounding=oracle.ROUND_TOWARD_ZERO)
     wq_o, ws_o = oracle.quantize_fp8(W, scaling, rounding=oracle.ROUND_TOWARD_ZERO)
     assert np.array_equal(down(hq), hq_o) and np.array_equal(down(wq), wq_o)
+    assert np.array_equal(down(ws).view(np.uint8), ws_o.view(np.uint8))
     assert np.array_equal(down(hs).view(np.uint8), hs_o.view(np.uint8))
     ids = np.random.default_rng(73).integers(0, V, size=T).astype(np.int32)
     out = acrl.acrl_score_pi_mu(h, w, hq, hs, wq, ws, scaling, up(torch, dev, ids))
