@@ -286,6 +286,61 @@ def test_long_workload_chunked():
     torch.cuda.empty_cache()
 
 
+def test_whole_sequences_q17b():
+    # Qwen-1.7B-shaped head (d=2048, V=151936, per-row FP8, 16 prompts x 8
+    # rollouts of up to 1024 tokens): the whole batch scored and reduced on the
+    # device; the two shortest sequences go through the oracle's full chain
+    # (its quantization, scores and reduce), token by token.  The binding bound
+    # is on the per-sequence sum of log-ratios: 1e-3 * sqrt(n_i).
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    w = inputs.WORKLOADS["q17b"]
+    T = inputs.n_valid(w)
+    slots = inputs.valid_slots(w)
+    n = inputs.lengths(w)
+    h = inputs.hidden_bf16_torch(w, T, dev)
+    W = inputs.weights_bf16_torch(w, dev)
+    hq, hs = acrl.acrl_quantize_fp8(h, w.scaling)
+    wq, ws = acrl.acrl_quantize_fp8(W, w.scaling)
+    ids_np = inputs.uniform_ids(w, T)
+    mask = inputs.mask(w)
+    groups = inputs.group_of_seq(w)
+    sc = acrl.acrl_score_pi_mu(h, W, hq, hs, wq, ws, w.scaling, up(torch, dev, ids_np),
+                               inv_temperature=w.inv_temperature, out_slot=up(torch, dev, slots),
+                               n_slots=w.slots)
+    red = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, sc["logp_pi"], sc["logp_mu"],
+                                       up(torch, dev, mask.reshape(-1)), up(torch, dev, groups),
+                                       entropy_pi=sc["entropy_pi"], entropy_mu=sc["entropy_mu"])
+    torch.cuda.synchronize()
+    seqs = np.argsort(n, kind="stable")[:2]
+    seq_of_row = slots // w.L
+    rows = np.concatenate([np.flatnonzero(seq_of_row == i) for i in seqs])
+    assert rows.size == n[seqs].sum()
+    Hs = h.index_select(0, torch.from_numpy(rows).to(dev)).cpu().view(torch.int16).numpy().view(np.uint16)
+    Wb = W.cpu().view(torch.int16).numpy().view(np.uint16)
+    hq_o, hs_o = oracle.quantize_fp8(Hs, w.scaling)   # per-row scales: each row's own
+    wq_o, ws_o = oracle.quantize_fp8(Wb, w.scaling)
+    ref = oracle.score(Hs, Wb, hq_o, hs_o, wq_o, ws_o, w.scaling, ids_np[rows], inv_temperature=w.inv_temperature)
+    got = {k: down(v)[slots[rows]] for k, v in sc.items()}
+    _compare(got, ref, w.V)
+    # the oracle's reduce over a batch of just these two sequences
+    lp_pi = np.zeros(2 * w.L)
+    lp_mu = np.zeros(2 * w.L)
+    sub_mask = mask[seqs]
+    lp_pi[np.flatnonzero(sub_mask.reshape(-1))] = ref["logp_pi"]
+    lp_mu[np.flatnonzero(sub_mask.reshape(-1))] = ref["logp_mu"]
+    oref = oracle.discrepancy_reduce(2, w.L, lp_pi, lp_mu, sub_mask, np.array([0, 1], np.int32), 2)
+    assert np.array_equal(down(red["seq_len"])[seqs], oref["seq_len"])
+    dsl = np.abs(down(red["seq_sum_logratio"])[seqs] - oref["seq_sum_logratio"])
+    assert np.all(dsl <= 1e-3 * np.sqrt(n[seqs])), dsl
+    # d = |p_pi - p_mu| moves by at most about p * |dlogp| per token
+    pmax = np.maximum(np.exp(lp_pi), np.exp(lp_mu)).reshape(2, w.L)
+    bound = 2 * 2 * TOL_LOGP * pmax.sum(axis=1) + 1e-12
+    assert np.all(np.abs(down(red["seq_sum_d"])[seqs] - oref["seq_sum_d"]) <= bound)
+    del h, W, hq, wq, sc
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("scaling", [oracle.PER_ROW, oracle.PER_TENSOR, oracle.MX32])
 def test_truncated_fp8_end_to_end(scaling):
     # the stress test's Q(x) = trunc(x/S) (Sec. 5.3): mu quantized toward
