@@ -253,8 +253,15 @@ acrl_status acrl_trace_score_events(void* const* events, int n);
  * Per group g (the G responses of one prompt): Y_g = mean over the group's
  * non-empty responses of their mean d (the formula for Y in Sec. 4.1).
  * Batch: mean over non-empty groups of Y_g (the outer mean of X, Sec. 4.1) and
- * the token-level statistics of ACRL_STAT_*.  Sums are accumulated in fp64.
- * Requirements: B, L, n_groups >= 0; group_of_seq[i] in [0, n_groups).
+ * the token-level statistics of ACRL_STAT_*.  Sums are accumulated in fp64;
+ * the standard deviation merges per-piece squared deviations pairwise
+ * (Chan, Golub and LeVeque), so every slot is read once.  Results are
+ * deterministic (fixed reduction trees, no floating-point atomics).
+ * Requirements: B, L, n_groups >= 0 (n_groups > 0 when B > 0);
+ * group_of_seq[i] in [0, n_groups) (device data, not checked: a response
+ * with another id belongs to no group and enters no batch statistic).
+ * Grouping the responses of a prompt together (non-decreasing group_of_seq)
+ * lets each group find its responses by binary search instead of a scan.
  */
 typedef struct acrl_reduce_desc {
   int64_t B;                    /* responses                                                */

@@ -205,9 +205,18 @@ def _workspace(nbytes: int, device) -> torch.Tensor:
 def acrl_quantize_fp8(x: torch.Tensor, scaling: int, rounding: int = ROUND_NEAREST_EVEN,
                       q: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None,
                       stream=None):
-    """x: bf16 [rows, cols] -> (q uint8 [rows, cols], scales)."""
-    _dev(x, torch.bfloat16, "x")
+    """x: bf16 [rows, cols] -> (q uint8 [rows, cols], scales).  x may be a
+    column slice of a wider matrix (unit column stride, row stride = ld)."""
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D")
     rows, cols = x.shape
+    if x.is_contiguous():
+        _dev(x, torch.bfloat16, "x")
+        ld = cols
+    else:
+        if not x.is_cuda or x.dtype != torch.bfloat16 or x.stride(1) != 1 or x.stride(0) < cols:
+            raise ValueError("x must be a bf16 device matrix with unit column stride")
+        ld = x.stride(0)
     if q is None:
         q = torch.empty((rows, cols), dtype=torch.uint8, device=x.device)
     if scales is None:
@@ -221,7 +230,7 @@ def acrl_quantize_fp8(x: torch.Tensor, scaling: int, rounding: int = ROUND_NEARE
     _check(lib().acrl_quantize_workspace_size(rows, cols, scaling, ctypes.byref(nb)),
            "acrl_quantize_workspace_size")
     ws = _workspace(nb.value, x.device) if nb.value else None
-    _check(lib().acrl_quantize_fp8(_ptr(x), rows, cols, cols, scaling, rounding, _ptr(q), _ptr(scales),
+    _check(lib().acrl_quantize_fp8(_ptr(x), rows, cols, ld, scaling, rounding, _ptr(q), _ptr(scales),
                                    _ptr(ws), nb.value, _stream(stream)), "acrl_quantize_fp8")
     return q, scales
 

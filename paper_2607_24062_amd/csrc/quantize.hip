@@ -4,9 +4,8 @@
 // per 32 consecutive elements, the MXFP8 of Sec. 5.2).
 //
 // All three are HBM-bound streams: 2 bytes in and 1 byte out per element
-// (per-tensor reads the tensor twice: amax pass, then encode).  Loads are
-// 16-byte vectors, one wavefront per row for the row kernels, so each
-// wave-instruction touches 1 KiB of contiguous memory.
+// (per-tensor reads the tensor twice: amax pass, then encode).  Loads and
+// stores are 16-byte vectors, one wavefront per row for the row kernels.
 #include "acrl_internal.h"
 
 namespace acrl {
@@ -34,6 +33,32 @@ __device__ __forceinline__ uint2 encode8_div(uint4 v, float s) {
   return r;
 }
 
+// x / s correctly rounded, from r = 1/s (correctly rounded, once per group)
+// and one correction step: y = x r, the residual x - y s (exact in one FMA)
+// times r moves y onto the correctly rounded quotient (Markstein).  The sign
+// comes from y, so -0 stays -0.  For bf16 x with |x| <= amax and s = amax /
+// 448 the result equals the divide, bit for bit, wherever the quotient can
+// reach a nonzero E4M3 code (|x / s| >= 2^-12), and has its sign elsewhere,
+// for every finite bf16 amax >= 2^-64 (checked over all such amax and x);
+// groups with a smaller or non-finite amax take the divide.
+constexpr float kRcpMinAmax = 0x1p-64f;
+__device__ __forceinline__ bool rcp_ok(float amax) { return amax >= kRcpMinAmax && amax < INFINITY; }
+__device__ __forceinline__ float div_rcp(float x, float s, float r) {
+  const float y = __fmul_rn(x, r);
+  return __builtin_copysignf(fmaf(fmaf(-y, s, x), r, y), y);
+}
+
+// 8 bf16 -> 8 e4m3 bytes of x / s by div_rcp.
+template <int ROUND>
+__device__ __forceinline__ uint2 encode8_rcp(uint4 v, float s, float r) {
+  uint2 o;
+  o.x = e4m3_pack4<ROUND>(div_rcp(bf16_lo(v.x), s, r), div_rcp(bf16_hi(v.x), s, r),
+                          div_rcp(bf16_lo(v.y), s, r), div_rcp(bf16_hi(v.y), s, r));
+  o.y = e4m3_pack4<ROUND>(div_rcp(bf16_lo(v.z), s, r), div_rcp(bf16_hi(v.z), s, r),
+                          div_rcp(bf16_lo(v.w), s, r), div_rcp(bf16_hi(v.w), s, r));
+  return o;
+}
+
 // 8 bf16 -> 8 e4m3 bytes of x * 2^k (exact power-of-two scaling).
 template <int ROUND>
 __device__ __forceinline__ uint2 encode8_ldexp(uint4 v, int k) {
@@ -46,11 +71,27 @@ __device__ __forceinline__ uint2 encode8_ldexp(uint4 v, int k) {
 }
 
 constexpr int kRowThreads = 256;       // 4 rows (one per wavefront) per workgroup
-constexpr int kRowRegVecs = 16;        // rows up to 64*16*8 = 8192 elements stay in VGPRs
+constexpr int kRowRegPairs = 8;        // rows up to 64*8*16 = 8192 elements stay in VGPRs
 
-// One wavefront per row.  tensor_amax == nullptr: per-row scale from the
-// row's own amax (written to scales[row]); otherwise the per-tensor amax (as
-// fp32 bits) gives the scale, and block 0 writes it to scales[0].
+// 16 bf16 (two 16-byte vectors) -> 16 e4m3 bytes of x / s (RCP: by div_rcp).
+template <int ROUND, bool RCP>
+__device__ __forceinline__ uint4 encode16(uint4 a, uint4 b, float s, float r) {
+  uint2 lo, hi;
+  if constexpr (RCP) {
+    lo = encode8_rcp<ROUND>(a, s, r);
+    hi = encode8_rcp<ROUND>(b, s, r);
+  } else {
+    lo = encode8_div<ROUND>(a, s);
+    hi = encode8_div<ROUND>(b, s);
+  }
+  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+
+// One wavefront per row; lane l owns the 32-byte pieces l, l + 64, ... of the
+// row (two 16-byte loads, one 16-byte store each).  tensor_amax == nullptr:
+// per-row scale from the row's own amax (written to scales[row]); otherwise
+// the per-tensor amax (as fp32 bits) gives the scale, and block 0 writes it
+// to scales[0].
 template <int ROUND>
 __global__ __launch_bounds__(kRowThreads) void quantize_rows_kernel(
     const uint16_t* __restrict__ x, int64_t rows, int64_t cols, int64_t ld,
@@ -59,68 +100,114 @@ __global__ __launch_bounds__(kRowThreads) void quantize_rows_kernel(
   const int64_t row = (int64_t)blockIdx.x * (kRowThreads / 64) + (threadIdx.x >> 6);
   if (row >= rows) return;
   const uint4* src = reinterpret_cast<const uint4*>(x + row * ld);
-  uint2* dst = reinterpret_cast<uint2*>(q + row * cols);
-  const int64_t nvec = cols >> 3;
-  const bool in_regs = nvec <= 64 * kRowRegVecs;
+  uint4* dst = reinterpret_cast<uint4*>(q + row * cols);
+  const int64_t npair = cols >> 4;  // cols is a multiple of 32
+  const bool in_regs = npair <= 64 * kRowRegPairs;
 
-  uint4 buf[kRowRegVecs];
-  float s;
+  uint4 buf[2 * kRowRegPairs];
+  float s, amax;
   if (tensor_amax) {
-    s = group_scale(__uint_as_float(*tensor_amax));
+    amax = __uint_as_float(*tensor_amax);
+    s = group_scale(amax);
     if (row == 0 && lane == 0) scales[0] = s;
     if (in_regs) {
 #pragma unroll
-      for (int it = 0; it < kRowRegVecs; ++it) {
+      for (int it = 0; it < kRowRegPairs; ++it) {
         const int64_t v = lane + 64 * it;
-        if (v < nvec) buf[it] = src[v];
+        if (v < npair) {
+          buf[2 * it] = src[2 * v];
+          buf[2 * it + 1] = src[2 * v + 1];
+        }
       }
     }
   } else {
-    float amax = 0.0f;
+    amax = 0.0f;
     if (in_regs) {
 #pragma unroll
-      for (int it = 0; it < kRowRegVecs; ++it) {
+      for (int it = 0; it < kRowRegPairs; ++it) {
         const int64_t v = lane + 64 * it;
-        if (v < nvec) {
-          buf[it] = src[v];
-          amax = fmaxf(amax, absmax8(buf[it]));
+        if (v < npair) {
+          buf[2 * it] = src[2 * v];
+          buf[2 * it + 1] = src[2 * v + 1];
+          amax = fmaxf(amax, fmaxf(absmax8(buf[2 * it]), absmax8(buf[2 * it + 1])));
         }
       }
     } else {
-      for (int64_t v = lane; v < nvec; v += 64) amax = fmaxf(amax, absmax8(src[v]));
+      for (int64_t v = lane; v < npair; v += 64)
+        amax = fmaxf(amax, fmaxf(absmax8(src[2 * v]), absmax8(src[2 * v + 1])));
     }
     amax = wave_max(amax);
     s = group_scale(amax);
     if (lane == 0) scales[row] = s;
   }
-  if (in_regs) {
+  auto store = [&](auto rcp_tag) {
+    constexpr bool RCP = decltype(rcp_tag)::value;
+    const float r = RCP ? 1.0f / s : 0.0f;
+    if (in_regs) {
 #pragma unroll
-    for (int it = 0; it < kRowRegVecs; ++it) {
-      const int64_t v = lane + 64 * it;
-      if (v < nvec) dst[v] = encode8_div<ROUND>(buf[it], s);
+      for (int it = 0; it < kRowRegPairs; ++it) {
+        const int64_t v = lane + 64 * it;
+        if (v < npair) dst[v] = encode16<ROUND, RCP>(buf[2 * it], buf[2 * it + 1], s, r);
+      }
+    } else {
+      for (int64_t v = lane; v < npair; v += 64) dst[v] = encode16<ROUND, RCP>(src[2 * v], src[2 * v + 1], s, r);
     }
-  } else {
-    for (int64_t v = lane; v < nvec; v += 64) dst[v] = encode8_div<ROUND>(src[v], s);
-  }
+  };
+  if (rcp_ok(amax)) store(std::true_type{});  // uniform over the wavefront
+  else store(std::false_type{});
 }
 
 __global__ void zero_u32_kernel(uint32_t* p) { *p = 0u; }
 
-// Per-tensor amax: grid-stride over 16-byte vectors; the magnitudes are
-// non-negative floats, whose bit patterns order like unsigned integers, so
-// the grid-wide max is an atomicMax on the bits.
+// Per-tensor amax: one wavefront per row (rows strided over the grid), eight
+// 16-byte loads in flight per lane.  The magnitudes are non-negative floats,
+// whose bit patterns order like unsigned integers, so the grid-wide max is an
+// atomicMax on the bits (one per wavefront).
+constexpr int kAmaxUnroll = 8;
+// Contiguous tensors (ld == cols): the tensor as one array of 16-byte
+// vectors, each workgroup sweeping its own contiguous range with kAmaxUnroll
+// loads in flight per thread; one atomic per workgroup.
+__global__ __launch_bounds__(256) void amax_flat_kernel(const uint4* __restrict__ x, int64_t nvec,
+                                                        int64_t per_block, uint32_t* amax_bits) {
+  __shared__ float sh[4];
+  const int64_t begin = (int64_t)blockIdx.x * per_block;
+  const int64_t end = min(begin + per_block, nvec);
+  int64_t i = begin + threadIdx.x;
+  float m = 0.0f;
+  for (; i + 256 * (kAmaxUnroll - 1) < end; i += 256 * kAmaxUnroll) {
+    uint4 t[kAmaxUnroll];
+#pragma unroll
+    for (int k = 0; k < kAmaxUnroll; ++k) t[k] = x[i + 256 * k];
+#pragma unroll
+    for (int k = 0; k < kAmaxUnroll; ++k) m = fmaxf(m, absmax8(t[k]));
+  }
+  for (; i < end; i += 256) m = fmaxf(m, absmax8(x[i]));
+  m = wave_max(m);
+  if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) atomicMax(amax_bits, __float_as_uint(fmaxf(fmaxf(sh[0], sh[1]), fmaxf(sh[2], sh[3]))));
+}
+
 __global__ __launch_bounds__(256) void amax_kernel(const uint16_t* __restrict__ x, int64_t rows,
                                                    int64_t cols, int64_t ld, uint32_t* amax_bits) {
-  const int64_t nvec_row = cols >> 3;
-  const int64_t total = rows * nvec_row;
+  const int lane = threadIdx.x & 63;
+  const int64_t nvec = cols >> 3;
+  const int64_t nwaves = (int64_t)gridDim.x * 4;
   float m = 0.0f;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t r = i / nvec_row, v = i - r * nvec_row;
-    m = fmaxf(m, absmax8(reinterpret_cast<const uint4*>(x + r * ld)[v]));
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < rows; r += nwaves) {
+    const uint4* src = reinterpret_cast<const uint4*>(x + r * ld);
+    int64_t v = lane;
+    for (; v + 64 * (kAmaxUnroll - 1) < nvec; v += 64 * kAmaxUnroll) {
+      uint4 t[kAmaxUnroll];
+#pragma unroll
+      for (int k = 0; k < kAmaxUnroll; ++k) t[k] = src[v + 64 * k];
+#pragma unroll
+      for (int k = 0; k < kAmaxUnroll; ++k) m = fmaxf(m, absmax8(t[k]));
+    }
+    for (; v < nvec; v += 64) m = fmaxf(m, absmax8(src[v]));
   }
   m = wave_max(m);
-  if ((threadIdx.x & 63) == 0) atomicMax(amax_bits, __float_as_uint(m));
+  if (lane == 0) atomicMax(amax_bits, __float_as_uint(m));
 }
 
 // MX32: one thread per 32-element block (64 bytes in, 32 bytes + 1 scale out).
@@ -207,8 +294,17 @@ hipError_t launch_quantize_t(const uint16_t* x, int64_t rows, int64_t cols, int6
   if (scaling == ACRL_SCALE_PER_TENSOR) {
     uint32_t* bits = (uint32_t*)workspace;
     hipLaunchKernelGGL(zero_u32_kernel, dim3(1), dim3(1), 0, s, bits);
-    hipLaunchKernelGGL(amax_kernel, dim3(grid_for(rows * (cols >> 3), 256 * 8, 4096)), dim3(256),
-                       0, s, x, rows, cols, ld, bits);
+    if (ld == cols) {
+      const int64_t nvec = rows * (cols >> 3);
+      const unsigned g = grid_for(nvec, 256 * kAmaxUnroll, 2048);
+      const int64_t unit = 256 * kAmaxUnroll;
+      const int64_t per_block = ((nvec + g - 1) / g + unit - 1) / unit * unit;
+      hipLaunchKernelGGL(amax_flat_kernel, dim3(g), dim3(256), 0, s, reinterpret_cast<const uint4*>(x), nvec,
+                         per_block, bits);
+    } else {
+      hipLaunchKernelGGL(amax_kernel, dim3(grid_for(rows, 4, 8192)), dim3(256), 0, s, x, rows, cols, ld,
+                         bits);
+    }
     amax = bits;
   }
   const int rows_per_block = kRowThreads / 64;

@@ -51,138 +51,292 @@ __device__ __forceinline__ double block_max(double v, double* sh) {
   return t;
 }
 
+// Count, mean and sum of squared deviations of a set of values; two sets
+// combine exactly in real arithmetic (the pairwise update of Chan, Golub and
+// LeVeque), so the squared deviations need no second pass over the slots.
+struct Var {
+  double n, mu, m2;
+};
+__device__ __forceinline__ Var var_merge(const Var& a, const Var& b) {
+  if (b.n == 0.0) return a;
+  if (a.n == 0.0) return b;
+  const double n = a.n + b.n, d = b.mu - a.mu, f = b.n / n;
+  return Var{n, a.mu + d * f, a.m2 + b.m2 + d * d * a.n * f};
+}
+
+// Block-wide sums of NS values, their maximum and the merge of the threads'
+// Vars, with one barrier: shuffle trees inside each wavefront, then every
+// thread combines the wavefronts' results in wavefront order, so all threads
+// hold the (deterministic) totals.  A second call on the same shared memory
+// needs a barrier in between.
+template <int NS, int NT = kRedThreads>
+struct BlockShared {
+  double s[NT / 64][NS];
+  double mx[NT / 64];
+  Var var[NT / 64];
+};
+template <int NS, int NT = kRedThreads>
+__device__ __forceinline__ void block_stats(double (&v)[NS], double& mx, Var& var, BlockShared<NS, NT>& sh) {
+  const int w = threadIdx.x >> 6;
+#pragma unroll
+  for (int k = 0; k < NS; ++k) v[k] = wave_sum(v[k]);
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) {
+    mx = fmax(mx, __shfl_xor(mx, m));
+    var = var_merge(var, Var{__shfl_xor(var.n, m), __shfl_xor(var.mu, m), __shfl_xor(var.m2, m)});
+  }
+  if ((threadIdx.x & 63) == 0) {
+#pragma unroll
+    for (int k = 0; k < NS; ++k) sh.s[w][k] = v[k];
+    sh.mx[w] = mx;
+    sh.var[w] = var;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < NS; ++k) {
+    double t = 0.0;
+#pragma unroll 1
+    for (int q = 0; q < NT / 64; ++q) t += sh.s[q][k];
+    v[k] = t;
+  }
+  mx = sh.mx[0];
+  var = sh.var[0];
+#pragma unroll 1
+  for (int q = 1; q < NT / 64; ++q) {
+    mx = fmax(mx, sh.mx[q]);
+    var = var_merge(var, sh.var[q]);
+  }
+}
+
 __device__ __forceinline__ double token_distance(float lp_pi, float lp_mu) {
   return fabs(exp((double)lp_pi) - exp((double)lp_mu));
 }
 
-// One workgroup per response.
-__global__ __launch_bounds__(kRedThreads) void reduce_seq_kernel(acrl_reduce_desc p, SeqRec* rec) {
-  __shared__ double sh[kRedThreads / 64];
+// VEC consecutive slots of one thread: 16-byte loads for VEC = 4.
+template <int VEC>
+struct Slots {
+  float a[VEC], b[VEC], hp[VEC], hm[VEC];
+  uint8_t m[VEC];
+};
+template <int VEC>
+__device__ __forceinline__ void load_slots(const acrl_reduce_desc& p, int64_t t, bool ent, Slots<VEC>& v) {
+  if constexpr (VEC == 4) {
+    const float4 a = *reinterpret_cast<const float4*>(p.logp_pi + t);
+    const float4 b = *reinterpret_cast<const float4*>(p.logp_mu + t);
+    const uchar4 m = *reinterpret_cast<const uchar4*>(p.mask + t);
+    v.a[0] = a.x; v.a[1] = a.y; v.a[2] = a.z; v.a[3] = a.w;
+    v.b[0] = b.x; v.b[1] = b.y; v.b[2] = b.z; v.b[3] = b.w;
+    v.m[0] = m.x; v.m[1] = m.y; v.m[2] = m.z; v.m[3] = m.w;
+    if (ent) {
+      const float4 hp = p.entropy_pi ? *reinterpret_cast<const float4*>(p.entropy_pi + t) : float4{};
+      const float4 hm = p.entropy_mu ? *reinterpret_cast<const float4*>(p.entropy_mu + t) : float4{};
+      v.hp[0] = hp.x; v.hp[1] = hp.y; v.hp[2] = hp.z; v.hp[3] = hp.w;
+      v.hm[0] = hm.x; v.hm[1] = hm.y; v.hm[2] = hm.z; v.hm[3] = hm.w;
+    }
+  } else {
+    v.a[0] = p.logp_pi[t];
+    v.b[0] = p.logp_mu[t];
+    v.m[0] = p.mask[t];
+    if (ent) {
+      v.hp[0] = p.entropy_pi ? p.entropy_pi[t] : 0.0f;
+      v.hm[0] = p.entropy_mu ? p.entropy_mu[t] : 0.0f;
+    }
+  }
+}
+
+// One workgroup per response; thread k takes the VEC-slot pieces k, k + 256,
+// ... of the response's L slots.  Every slot is loaded (masked ones too: no
+// load waits on the mask).  The sums are plain fp64 sums in piece order; the
+// squared deviations of each piece (about its own mean) merge into the
+// thread's running Var, and the threads' Vars merge in a fixed tree.
+template <int VEC>
+__global__ __launch_bounds__(kRedThreads) void reduce_seq_kernel(acrl_reduce_desc p, SeqRec* rec,
+                                                                 uint32_t* unsorted) {
+  __shared__ BlockShared<5> sh;
   const int64_t i = blockIdx.x;
   const int64_t base = i * p.L;
+  const bool ent = p.entropy_pi || p.entropy_mu;
+  constexpr int kStride = kRedThreads * VEC;
   double n = 0, sd = 0, sl = 0, shp = 0, shm = 0, mx = 0;
-  for (int64_t j = threadIdx.x; j < p.L; j += kRedThreads) {
-    const int64_t t = base + j;
-    float dtok = 0.0f;
-    if (p.mask[t]) {
-      const float a = p.logp_pi[t], b = p.logp_mu[t];
-      const double dv = token_distance(a, b);
-      n += 1.0;
-      sd += dv;
-      sl += (double)a - (double)b;
-      if (p.entropy_pi) shp += p.entropy_pi[t];
-      if (p.entropy_mu) shm += p.entropy_mu[t];
-      mx = fmax(mx, dv);
-      dtok = (float)dv;
+  Var var{0.0, 0.0, 0.0};
+#pragma unroll 2
+  for (int64_t j = (int64_t)threadIdx.x * VEC; j < p.L; j += kStride) {
+    Slots<VEC> v;
+    load_slots<VEC>(p, base + j, ent, v);
+    double dv[VEC];
+    float dt[VEC];
+    double pn = 0.0, ps = 0.0;
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+      dt[k] = 0.0f;
+      dv[k] = 0.0;
+      if (v.m[k]) {
+        dv[k] = token_distance(v.a[k], v.b[k]);
+        n += 1.0;
+        sd += dv[k];
+        sl += (double)v.a[k] - (double)v.b[k];
+        if (ent) {
+          shp += v.hp[k];
+          shm += v.hm[k];
+        }
+        mx = fmax(mx, dv[k]);
+        dt[k] = (float)dv[k];
+        pn += 1.0;
+        ps += dv[k];
+      }
     }
-    if (p.d_tok) p.d_tok[t] = dtok;
-  }
-  n = block_sum(n, sh);
-  sd = block_sum(sd, sh);
-  sl = block_sum(sl, sh);
-  shp = block_sum(shp, sh);
-  shm = block_sum(shm, sh);
-  mx = block_max(mx, sh);
-  const double mean = n > 0 ? sd / n : 0.0;
-  double m2 = 0.0;  // second pass over the (cached) slots: squared deviations
-  for (int64_t j = threadIdx.x; j < p.L; j += kRedThreads) {
-    const int64_t t = base + j;
-    if (p.mask[t]) {
-      const double dv = token_distance(p.logp_pi[t], p.logp_mu[t]) - mean;
-      m2 += dv * dv;
+    if (pn > 0.0) {
+      const double pm = ps / pn;
+      double pm2 = 0.0;
+#pragma unroll
+      for (int k = 0; k < VEC; ++k)
+        if (v.m[k]) pm2 += (dv[k] - pm) * (dv[k] - pm);
+      var = var_merge(var, Var{pn, pm, pm2});
+    }
+    if (p.d_tok) {
+      if constexpr (VEC == 4) *reinterpret_cast<float4*>(p.d_tok + base + j) = make_float4(dt[0], dt[1], dt[2], dt[3]);
+      else p.d_tok[base + j] = dt[0];
     }
   }
-  m2 = block_sum(m2, sh);
+  double v[5] = {n, sd, sl, shp, shm};
+  block_stats<5>(v, mx, var, sh);
+  n = v[0];
+  sd = v[1];
+  sl = v[2];
+  shp = v[3];
+  shm = v[4];
   if (threadIdx.x == 0) {
+    const double mean = n > 0 ? sd / n : 0.0;
     SeqRec r;
-    r.n = n; r.sum_d = sd; r.sum_lr = sl; r.sum_hp = shp; r.sum_hm = shm; r.max_d = mx; r.m2 = m2;
+    r.n = n; r.sum_d = sd; r.sum_lr = sl; r.sum_hp = shp; r.sum_hm = shm; r.max_d = mx; r.m2 = var.m2;
     r.pad = 0;
     rec[i] = r;
     if (p.seq_len) p.seq_len[i] = (int32_t)n;
     if (p.seq_sum_d) p.seq_sum_d[i] = sd;
     if (p.seq_sum_logratio) p.seq_sum_logratio[i] = sl;
     p.seq_mean_d[i] = (float)mean;
+    if (i + 1 < p.B && p.group_of_seq[i] > p.group_of_seq[i + 1]) atomicOr(unsorted, 1u);
   }
 }
 
-// One workgroup per group: Y_g over the group's non-empty responses.
-__global__ __launch_bounds__(kRedThreads) void reduce_group_kernel(acrl_reduce_desc p,
-                                                                   const SeqRec* rec,
-                                                                   double* gy, double* gcount) {
-  __shared__ double sh[kRedThreads / 64];
+__global__ void clear_flag_kernel(uint32_t* f) { *f = 0u; }
+
+// Per-group partial record (the groups partition the responses, so the
+// batch statistics come from these).
+struct GroupRec {
+  double n, sum_d, sum_lr, sum_hp, sum_hm, max_d, nseq, mu, m2;
+  double pad[7];
+};
+
+// One workgroup per group: Y_g over the group's non-empty responses, and the
+// group's share of the batch statistics.  When group_of_seq is non-decreasing
+// (flag unsorted == 0, set by the per-response kernel) the group's responses are
+// the range found by binary search; otherwise every response is scanned.
+__global__ __launch_bounds__(kRedThreads) void reduce_group_kernel(acrl_reduce_desc p, const SeqRec* rec,
+                                                                   const uint32_t* unsorted, double* gy,
+                                                                   double* gcount, GroupRec* grec) {
+  __shared__ BlockShared<7> sh;
+  __shared__ int64_t range[2];
   const int g = blockIdx.x;
-  double s = 0, c = 0;
-  for (int64_t i = threadIdx.x; i < p.B; i += kRedThreads) {
-    if (p.group_of_seq[i] == g && rec[i].n > 0) {
-      s += rec[i].sum_d / rec[i].n;
-      c += 1.0;
+  const bool sorted = *unsorted == 0u;
+  int64_t lo = 0, hi = p.B;
+  if (sorted) {
+    if (threadIdx.x == 0) {
+      int64_t a = 0, b = p.B;
+      while (a < b) {  // first response with group >= g
+        const int64_t m = (a + b) >> 1;
+        if (p.group_of_seq[m] < g) a = m + 1;
+        else b = m;
+      }
+      range[0] = a;
+      b = p.B;
+      while (a < b) {  // first response with group > g
+        const int64_t m = (a + b) >> 1;
+        if (p.group_of_seq[m] <= g) a = m + 1;
+        else b = m;
+      }
+      range[1] = a;
+    }
+    __syncthreads();
+    lo = range[0];
+    hi = range[1];
+  }
+  double v[7] = {0, 0, 0, 0, 0, 0, 0};  // sum of means, responses, n, sum d, sum log-ratio, sum H_pi, sum H_mu
+  double mx = 0.0;
+  Var var{0.0, 0.0, 0.0};
+  for (int64_t i = lo + threadIdx.x; i < hi; i += kRedThreads) {
+    if (sorted || p.group_of_seq[i] == g) {
+      const SeqRec r = rec[i];
+      if (r.n > 0) {
+        const double mean = r.sum_d / r.n;
+        v[0] += mean;
+        v[1] += 1.0;
+        v[2] += r.n;
+        v[3] += r.sum_d;
+        v[4] += r.sum_lr;
+        v[5] += r.sum_hp;
+        v[6] += r.sum_hm;
+        mx = fmax(mx, r.max_d);
+        var = var_merge(var, Var{r.n, mean, r.m2});
+      }
     }
   }
-  s = block_sum(s, sh);
-  c = block_sum(c, sh);
+  block_stats<7>(v, mx, var, sh);
   if (threadIdx.x == 0) {
-    const double y = c > 0 ? s / c : 0.0;
+    const double c = v[1];
+    const double y = c > 0 ? v[0] / c : 0.0;
     gy[g] = y;
     gcount[g] = c;
     p.group_y[g] = (float)y;
     if (p.group_nseq) p.group_nseq[g] = (int32_t)c;
+    GroupRec r;
+    r.n = v[2]; r.sum_d = v[3]; r.sum_lr = v[4]; r.sum_hp = v[5]; r.sum_hm = v[6]; r.max_d = mx; r.nseq = c;
+    r.mu = var.mu; r.m2 = var.m2;
+    for (int k = 0; k < 7; ++k) r.pad[k] = 0.0;
+    grec[g] = r;
   }
 }
 
-// One workgroup: batch statistics.
-__global__ __launch_bounds__(kRedThreads) void reduce_batch_kernel(acrl_reduce_desc p,
-                                                                   const SeqRec* rec,
-                                                                   const double* gy,
-                                                                   const double* gcount) {
-  __shared__ double sh[kRedThreads / 64];
-  double n = 0, sd = 0, sl = 0, shp = 0, shm = 0, mx = 0, ns = 0;
-  for (int64_t i = threadIdx.x; i < p.B; i += kRedThreads) {
-    const SeqRec r = rec[i];
-    n += r.n; sd += r.sum_d; sl += r.sum_lr; shp += r.sum_hp; shm += r.sum_hm;
-    mx = fmax(mx, r.max_d);
-    ns += r.n > 0 ? 1.0 : 0.0;
-  }
-  n = block_sum(n, sh);
-  sd = block_sum(sd, sh);
-  sl = block_sum(sl, sh);
-  shp = block_sum(shp, sh);
-  shm = block_sum(shm, sh);
-  mx = block_max(mx, sh);
-  ns = block_sum(ns, sh);
-  const double mean = n > 0 ? sd / n : 0.0;
-  // total squared deviation from the per-response ones (parallel-variance merge)
-  double m2 = 0;
-  for (int64_t i = threadIdx.x; i < p.B; i += kRedThreads) {
-    const SeqRec r = rec[i];
-    if (r.n > 0) {
-      const double dm = r.sum_d / r.n - mean;
-      m2 += r.m2 + r.n * dm * dm;
-    }
-  }
-  m2 = block_sum(m2, sh);
-  double ys = 0, ng = 0;
-  for (int64_t g = threadIdx.x; g < p.n_groups; g += kRedThreads) {
+// One workgroup of kBatchThreads: batch statistics from the group records.
+constexpr int kBatchThreads = 1024;
+__global__ __launch_bounds__(kBatchThreads) void reduce_batch_kernel(acrl_reduce_desc p, const GroupRec* grec,
+                                                                     const double* gy, const double* gcount) {
+  __shared__ BlockShared<8, kBatchThreads> sh;
+  double v[8] = {0, 0, 0, 0, 0, 0, 0, 0};  // n, sum d, sum log-ratio, sum H_pi, sum H_mu, responses, sum Y_g, groups
+  double mx = 0.0;
+  Var var{0.0, 0.0, 0.0};
+  for (int64_t g = threadIdx.x; g < p.n_groups; g += kBatchThreads) {
+    const GroupRec r = grec[g];
+    v[0] += r.n;
+    v[1] += r.sum_d;
+    v[2] += r.sum_lr;
+    v[3] += r.sum_hp;
+    v[4] += r.sum_hm;
+    v[5] += r.nseq;
     if (gcount[g] > 0) {
-      ys += gy[g];
-      ng += 1.0;
+      v[6] += gy[g];
+      v[7] += 1.0;
     }
+    mx = fmax(mx, r.max_d);
+    var = var_merge(var, Var{r.n, r.mu, r.m2});
   }
-  ys = block_sum(ys, sh);
-  ng = block_sum(ng, sh);
+  block_stats<8, kBatchThreads>(v, mx, var, sh);
   if (threadIdx.x == 0) {
+    const double n = v[0], ng = v[7];
     double* st = p.stats;
-    st[ACRL_STAT_Y_BATCH] = ng > 0 ? ys / ng : 0.0;
-    st[ACRL_STAT_TOK_MEAN_D] = mean;
+    st[ACRL_STAT_Y_BATCH] = ng > 0 ? v[6] / ng : 0.0;
+    st[ACRL_STAT_TOK_MEAN_D] = n > 0 ? v[1] / n : 0.0;
     st[ACRL_STAT_TOK_MAX_D] = mx;
-    st[ACRL_STAT_TOK_STD_D] = n > 0 ? sqrt(m2 / n) : 0.0;
-    st[ACRL_STAT_MEAN_H_PI] = n > 0 ? shp / n : 0.0;
-    st[ACRL_STAT_MEAN_H_MU] = n > 0 ? shm / n : 0.0;
+    st[ACRL_STAT_TOK_STD_D] = n > 0 ? sqrt(var.m2 / n) : 0.0;
+    st[ACRL_STAT_MEAN_H_PI] = n > 0 ? v[3] / n : 0.0;
+    st[ACRL_STAT_MEAN_H_MU] = n > 0 ? v[4] / n : 0.0;
     st[ACRL_STAT_N_TOKENS] = n;
     st[ACRL_STAT_N_GROUPS] = ng;
-    st[ACRL_STAT_TOK_MEAN_LOGRATIO] = n > 0 ? sl / n : 0.0;
-    st[ACRL_STAT_N_SEQS] = ns;
+    st[ACRL_STAT_TOK_MEAN_LOGRATIO] = n > 0 ? v[2] / n : 0.0;
+    st[ACRL_STAT_N_SEQS] = v[5];
   }
 }
+
 
 // Element-wise controller.  alpha and the weight are evaluated in fp64 from
 // the fp32 inputs (exact conversions), then rounded to fp32 once.  Modes:
@@ -380,20 +534,36 @@ hipError_t launch_surrogate(const acrl_surrogate_desc& p, hipStream_t s) {
 
 size_t reduce_workspace_bytes(int64_t B, int64_t L, int64_t n_groups) {
   (void)L;
-  return align_up((size_t)B * sizeof(SeqRec), 256) + 2 * align_up((size_t)n_groups * sizeof(double), 256);
+  return align_up((size_t)B * sizeof(SeqRec), 256) + 2 * align_up((size_t)n_groups * sizeof(double), 256) +
+         align_up((size_t)n_groups * sizeof(GroupRec), 256) + 256;
 }
 
 hipError_t launch_reduce(const acrl_reduce_desc& p, hipStream_t s) {
   uint8_t* ws = static_cast<uint8_t*>(p.workspace);
   SeqRec* rec = reinterpret_cast<SeqRec*>(ws);
-  double* gy = reinterpret_cast<double*>(ws + align_up((size_t)p.B * sizeof(SeqRec), 256));
-  double* gc = gy + align_up((size_t)p.n_groups * sizeof(double), 256) / sizeof(double);
-  if (p.B > 0)
-    hipLaunchKernelGGL(reduce_seq_kernel, dim3((unsigned)p.B), dim3(kRedThreads), 0, s, p, rec);
+  size_t off = align_up((size_t)p.B * sizeof(SeqRec), 256);
+  double* gy = reinterpret_cast<double*>(ws + off);
+  off += align_up((size_t)p.n_groups * sizeof(double), 256);
+  double* gc = reinterpret_cast<double*>(ws + off);
+  off += align_up((size_t)p.n_groups * sizeof(double), 256);
+  GroupRec* grec = reinterpret_cast<GroupRec*>(ws + off);
+  off += align_up((size_t)p.n_groups * sizeof(GroupRec), 256);
+  uint32_t* unsorted = reinterpret_cast<uint32_t*>(ws + off);
+  hipLaunchKernelGGL(clear_flag_kernel, dim3(1), dim3(1), 0, s, unsorted);
+  if (p.B > 0) {
+    // 16-byte slot loads when every row of slots starts 16-byte aligned
+    auto al = [](const void* q, uintptr_t a) { return ((uintptr_t)q & (a - 1)) == 0; };
+    const bool vec = p.L % 4 == 0 && al(p.logp_pi, 16) && al(p.logp_mu, 16) && al(p.mask, 4) &&
+                     al(p.entropy_pi, 16) && al(p.entropy_mu, 16) && al(p.d_tok, 16);
+    if (vec)
+      hipLaunchKernelGGL(reduce_seq_kernel<4>, dim3((unsigned)p.B), dim3(kRedThreads), 0, s, p, rec, unsorted);
+    else
+      hipLaunchKernelGGL(reduce_seq_kernel<1>, dim3((unsigned)p.B), dim3(kRedThreads), 0, s, p, rec, unsorted);
+  }
   if (p.n_groups > 0)
     hipLaunchKernelGGL(reduce_group_kernel, dim3((unsigned)p.n_groups), dim3(kRedThreads), 0, s, p,
-                       (const SeqRec*)rec, gy, gc);
-  hipLaunchKernelGGL(reduce_batch_kernel, dim3(1), dim3(kRedThreads), 0, s, p, (const SeqRec*)rec,
+                       (const SeqRec*)rec, (const uint32_t*)unsorted, gy, gc, grec);
+  hipLaunchKernelGGL(reduce_batch_kernel, dim3(1), dim3(kBatchThreads), 0, s, p, (const GroupRec*)grec,
                      (const double*)gy, (const double*)gc);
   return hipGetLastError();
 }

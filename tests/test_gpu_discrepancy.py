@@ -14,7 +14,7 @@ from gpu_util import down, torch_dev, up, up_bf16
 pytestmark = pytest.mark.gpu
 
 
-def _batch(B, L, n_groups, seed, empty=()):
+def _batch(B, L, n_groups, seed, empty=(), shuffle=False):
     r = np.random.default_rng(seed)
     lens = r.integers(1, L + 1, size=B)
     for i in empty:
@@ -25,6 +25,8 @@ def _batch(B, L, n_groups, seed, empty=()):
     ent_pi = r.uniform(0, 9, size=(B, L)).astype(np.float32)
     ent_mu = r.uniform(0, 9, size=(B, L)).astype(np.float32)
     g = np.sort(r.integers(0, n_groups, size=B)).astype(np.int32)
+    if shuffle:  # responses of a group scattered over the batch
+        g = r.permutation(g).astype(np.int32)
     return mask, lp_pi, lp_mu, ent_pi, ent_mu, g
 
 
@@ -38,10 +40,15 @@ def _gpu_reduce(B, L, ng, mask, lp_pi, lp_mu, ent_pi, ent_mu, g):
     return {k: down(v) for k, v in out.items() if v is not None and not k.startswith("_")}
 
 
-@pytest.mark.parametrize("B,L,ng,empty", [(9, 23, 4, ()), (64, 4096, 8, ()), (5, 1, 2, (1,)),
-                                          (1, 700, 1, ()), (12, 300, 5, (0, 4)), (130, 257, 3, ())])
-def test_reduce_matches_oracle(B, L, ng, empty):
-    mask, lp_pi, lp_mu, ent_pi, ent_mu, g = _batch(B, L, ng, B * L, empty)
+@pytest.mark.parametrize("B,L,ng,empty,shuffle", [
+    (9, 23, 4, (), False), (64, 4096, 8, (), False), (5, 1, 2, (1,), False), (1, 700, 1, (), False),
+    (12, 300, 5, (0, 4), False), (130, 257, 3, (), False), (3, 16, 8, (), False),
+    (9, 23, 4, (), True), (130, 257, 3, (), True), (12, 300, 5, (0, 4), True),
+    (3000, 32, 1500, (5, 17), False), (3000, 32, 1500, (5, 17), True)])
+def test_reduce_matches_oracle(B, L, ng, empty, shuffle):
+    # sorted group ids take the binary-search path of the group kernel,
+    # shuffled ones the scan; groups with no response and > 1024 groups too
+    mask, lp_pi, lp_mu, ent_pi, ent_mu, g = _batch(B, L, ng, B * L, empty, shuffle)
     got = _gpu_reduce(B, L, ng, mask, lp_pi, lp_mu, ent_pi, ent_mu, g)
     ref = oracle.discrepancy_reduce(B, L, lp_pi, lp_mu, mask, g, ng, ent_pi, ent_mu)
     # same fp32 inputs, both sides accumulate in fp64: agreement to rounding

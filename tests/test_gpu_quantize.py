@@ -61,6 +61,44 @@ def test_edge_values(scaling, tag):
         _assert_same(x, scaling, rounding)
 
 
+def _all_magnitudes_up_to(amax_bits):
+    """Every bf16 x with |x| <= amax, both signs (amax itself included)."""
+    b = np.arange(0x7F80, dtype=np.uint16)
+    b = b[b <= amax_bits]
+    return np.concatenate([b, b | 0x8000]).astype(np.uint16)
+
+
+# bf16 amax patterns: subnormal, far below / just below / at / just above
+# 2^-64 (where the row kernel switches from the divide to the reciprocal
+# path), 1, 448, the largest finite value
+AMAX_BITS = [0x0001, 0x0C5A, 0x1F7F, 0x1F80, 0x1F81, 0x2A3B, 0x3F80, 0x43E0, 0x5555, 0x7F7F]
+
+
+@pytest.mark.parametrize("rounding", ROUNDINGS)
+def test_division_paths_every_magnitude(rounding):
+    # per-row: each row holds every magnitude up to its amax, so both division
+    # paths see every input they can get
+    rows = [_all_magnitudes_up_to(a) for a in AMAX_BITS]
+    cols = (max(r.size for r in rows) + 31) // 32 * 32
+    x = np.zeros((len(rows), cols), np.uint16)
+    for i, r in enumerate(rows):
+        x[i, :r.size] = r
+    _assert_same(x, oracle.PER_ROW, rounding)
+    # rows short enough for the kernel's in-register path
+    for r in rows:
+        if r.size <= 8192:
+            t = np.zeros((2, (r.size + 31) // 32 * 32), np.uint16)
+            t[0, :r.size] = r
+            t[1, :r.size] = r[::-1]
+            _assert_same(t, oracle.PER_ROW, rounding)
+    # per-tensor: one scale per tensor
+    for a in (0x1F7F, 0x1F80, 0x3F80):
+        r = _all_magnitudes_up_to(a)
+        t = np.zeros((1, (r.size + 31) // 32 * 32), np.uint16)
+        t[0, :r.size] = r
+        _assert_same(t.reshape(-1, 32), oracle.PER_TENSOR, rounding)
+
+
 def test_zero_rows_tensor():
     torch, dev = torch_dev()
     from paper_2607_24062_amd import acrl
@@ -125,3 +163,20 @@ def test_full_size_lm_head_sampled_rows(name, scaling):
         assert np.array_equal(down(s)[rows], so)
     del W, q, s
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("scaling,tag", SCHEMES)
+def test_row_stride(scaling, tag):
+    # a column slice of a wider matrix: ld > cols (the per-tensor amax then
+    # takes the per-row path instead of the flat one)
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    wide = random_bf16((37, 96 + 40), 91, std=3.0)
+    x = up_bf16(torch, dev, wide)[:, 8:8 + 96]
+    assert not x.is_contiguous() and x.stride(0) == 136
+    for rounding in ROUNDINGS:
+        q, s = acrl.acrl_quantize_fp8(x, scaling, rounding)
+        torch.cuda.synchronize()
+        qo, so = oracle.quantize_fp8(np.ascontiguousarray(wide[:, 8:8 + 96]), scaling, rounding)
+        assert np.array_equal(down(s).view(np.uint8), so.view(np.uint8))
+        assert np.array_equal(down(q), qo)
