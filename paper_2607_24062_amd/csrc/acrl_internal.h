@@ -33,6 +33,7 @@ struct ScorePlan {
   size_t ws_part_offset[2];  // byte offsets of the (M, S, U) partials of pi / mu
   size_t ws_logit_offset[2]; // byte offsets of the sampled-token logits of pi / mu
   size_t ws_pack_offset[4];  // byte offsets of the packed W, H (bf16) and Wq, Hq (e4m3)
+  size_t ws_mx_offset[2];    // MX: packed E8M0 scale images of Wq and Hq
   size_t ws_best_offset;     // sampling: the strips' best key, logit and row
   int div_tiles;             // full-vocabulary measures: token tiles per pass (0 = not planned)
   size_t ws_zbuf_offset[2];  //   the logits of pi and mu of one pass

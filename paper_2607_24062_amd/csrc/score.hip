@@ -77,8 +77,8 @@ struct ScoreParams {
   int n_tblocks;
   const float* a_scale;    // FP8 per-row: [V]; per-tensor: [1]
   const float* b_scale;    // FP8 per-row: [n_rows]; per-tensor: [1]
-  const uint8_t* a_mx;     // MX: E8M0 [V, d/32]
-  const uint8_t* b_mx;     // MX: E8M0 [n_rows, d/32]
+  const uint8_t* a_mx;     // MX: packed E8M0 image of W's scales (pack_mx_kernel)
+  const uint8_t* b_mx;     // MX: packed E8M0 image of H's scales
   int mx_row_bytes;        // d / 32
   float inv_temp;
   const int32_t* ids;
@@ -213,21 +213,23 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // Operand stages in LDS (one 64-byte K chunk of every row of both tiles per
-// stage).  MX also streams a small stage of E8M0 scales per chunk, and the
-// per-row FP8 mode keeps the weight-row scales of the last NS + 1 vocabulary
-// tiles (a tile's scales arrive with its first chunk, up to NS chunks before
-// the previous tile's epilogue reads its own), so both keep one operand
-// stage less.
+// stage).  MX also streams the E8M0 scales of the chunk's two MX blocks with
+// each stage (2 bytes per row of both tiles, 1 KiB, from the packed scale
+// images), and the per-row FP8 mode keeps the weight-row scales of the last
+// NS + 1 vocabulary tiles (a tile's scales arrive with its first chunk, up to
+// NS chunks before the previous tile's epilogue reads its own), so both keep
+// one operand stage less.
 template <int MODE>
 struct Pipe {
   static constexpr int kStages = (MODE == kMX || MODE == kFP8Row) ? 4 : 5;
-  static constexpr int kScaleBytes = (MODE == kMX) ? (kTileV + kTileT) * 4 : 0;  // per stage
+  static constexpr int kScaleBytes = (MODE == kMX) ? (kTileV + kTileT) * 2 : 0;  // per stage
   static constexpr int kRowScaleSlots = kStages + 1;
   static constexpr int kRowScaleBytes = (MODE == kFP8Row) ? kRowScaleSlots * kTileV * 4 : 0;
-  // buffer -> LDS loads per chunk per wave, at least: the two 16 KiB tile
-  // images spread over NW waves (1 KiB per load), plus the MX scales
+  // buffer -> LDS loads per chunk per wave: the two 16 KiB tile images spread
+  // over NW waves (1 KiB per load), plus one quarter of the MX scales (4
+  // bytes per lane)
   template <int NW>
-  static constexpr int loads_per_chunk() { return 2 * (16 / NW) + (MODE == kMX ? 2 : 0); }
+  static constexpr int loads_per_chunk() { return 2 * (16 / NW) + (MODE == kMX ? 1 : 0); }
 };
 
 // NW = 4: one wave per SIMD, each wave 128 vocabulary rows x 128 tokens
@@ -248,6 +250,7 @@ void score_kernel(ScoreParams p) {
   constexpr int SB = Pipe<MODE>::kScaleBytes;
   constexpr int LPC = Pipe<MODE>::template loads_per_chunk<NW>();
   constexpr int RSB = Pipe<MODE>::kRowScaleBytes;
+  static_assert(MODE != kMX || NW == 4, "the MX scale stream is spread over 4 waves");
   __shared__ __attribute__((aligned(1024))) uint8_t lds[NS * (kStageBytes + SB) + RSB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -369,19 +372,14 @@ void score_kernel(ScoreParams p) {
       }
     }
     if constexpr (MODE == kMX) {
-      // the E8M0 scales of MX blocks 2kc, 2kc+1 of each row: the aligned
-      // dword holding them (blocks 4(kc/2) .. 4(kc/2)+3; rows hold d/32 scale
-      // bytes, a multiple of 4), one dword per row, lane l of wave w moving
-      // row 64w + l of each tile.  The chunk's two bytes sit at byte
-      // 2 (kc % 2) of the dword.
-      const uint32_t mrb = (uint32_t)p.mx_row_bytes;
-      const __amdgpu_buffer_rsrc_t sa = make_rsrc(p.a_mx + (int64_t)v0 * p.mx_row_bytes, (uint32_t)a_rows * mrb);
-      const __amdgpu_buffer_rsrc_t sb = make_rsrc(p.b_mx + (int64_t)t0 * p.mx_row_bytes, (uint32_t)b_rows * mrb);
-      const uint32_t soff = (uint32_t)(kc >> 1) * 4;
-      if (NW == 4 || wave_u < 4) buffer_to_lds<4>(sa, (uint32_t)min(wave_u * 64 + lane, a_rows - 1) * mrb, soff,
-                       scales_at(stg) + wave_u * 64 * 4);
-      if (NW == 4 || wave_u < 4) buffer_to_lds<4>(sb, (uint32_t)min(wave_u * 64 + lane, b_rows - 1) * mrb, soff,
-                       scales_at(stg) + (kTileV + wave_u * 64) * 4);
+      // the chunk's E8M0 scales (MX blocks 2kc, 2kc+1: 2 bytes per row) of
+      // the 256 W rows (waves 0, 1) and the 256 H rows (waves 2, 3), 256
+      // contiguous bytes per wave in the packed scale images
+      const uint32_t tmx = (uint32_t)kTileV * (uint32_t)p.mx_row_bytes;  // bytes of one tile's image
+      const __amdgpu_buffer_rsrc_t rs = wave_u < 2 ? make_rsrc(p.a_mx + (int64_t)(vt_begin + q) * tmx, tmx)
+                                                   : make_rsrc(p.b_mx + (int64_t)ttg * tmx, tmx);
+      buffer_to_lds<4>(rs, (uint32_t)lane * 4u, (uint32_t)kc * 512u + (uint32_t)(wave_u & 1) * 256u,
+                       scales_at(stg) + wave_u * 256);
     }
   };
 
@@ -427,16 +425,14 @@ void score_kernel(ScoreParams p) {
       else bf[j] = read16x2(row);
     }
   };
-  // MX scales of the chunk in stage stg: every tile has an even number of
-  // chunks (d is a multiple of 128) and NS is even, so the chunk's position
-  // in its tile has the parity of stg; lane group g takes block 2kc + g.
-  static_assert(MODE != kMX || NS % 2 == 0, "MX scale parity needs an even stage count");
+  // MX scales of the chunk in stage stg: 2 bytes per row (W rows, then H
+  // rows); lane group g takes block 2kc + g.
   auto read_sa = [&](int stg, int grp) -> int {
-    return scales_at(stg)[(wv * 128 + (grp & 3) * 32 + r32) * 4 + (stg & 1) * 2 + g];
+    return scales_at(stg)[(wv * 128 + (grp & 3) * 32 + r32) * 2 + g];
   };
   auto read_sb = [&](int stg, int (&sb)[JT]) {
 #pragma unroll
-    for (int j = 0; j < JT; ++j) sb[j] = scales_at(stg)[(kTileV + wt * TW + j * 32 + r32) * 4 + (stg & 1) * 2 + g];
+    for (int j = 0; j < JT; ++j) sb[j] = scales_at(stg)[(kTileV + wt * TW + j * 32 + r32) * 2 + g];
   };
   auto mfma_group = [&](int grp, const FragT& fa, const FragT (&fb)[JT], int sa, const int (&sb)[JT]) {
     const int bb = grp & 3;
@@ -923,6 +919,31 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint8_t* __restrict__ s
   }
 }
 
+// Packed MX scale image read by score_kernel: for each 256-row tile and each
+// 64-byte chunk kc, the E8M0 scales of MX blocks 2kc, 2kc+1 of the tile's
+// 256 rows in row order (2 bytes per row, 512 bytes).  Rows past `rows`
+// repeat the last row.  One thread per row and chunk; `units` = n_tiles *
+// 256 * n_chunks < 2^32.
+__global__ __launch_bounds__(256) void pack_mx_kernel(const uint16_t* __restrict__ src, uint32_t rows,
+                                                      uint32_t n_chunks, uint32_t units, uint16_t* __restrict__ dst) {
+  for (uint32_t u = blockIdx.x * blockDim.x + threadIdx.x; u < units; u += gridDim.x * blockDim.x) {
+    const uint32_t rr = u % kTileV, tc = u / kTileV;  // tc = tile * n_chunks + kc
+    const uint32_t tile = tc / n_chunks, kc = tc - tile * n_chunks;
+    const uint32_t row = tile * kTileV + rr;
+    const uint32_t sr = row < rows ? row : rows - 1;
+    dst[u] = src[(size_t)sr * n_chunks + kc];
+  }
+}
+
+inline void launch_pack_mx(const void* scales, int64_t rows, int64_t d, int64_t n_tiles, uint8_t* dst,
+                           hipStream_t s) {
+  const int64_t n_chunks = d / kChunk;  // a row holds d / 32 scale bytes = 2 per chunk
+  const int64_t units = n_tiles * kTileV * n_chunks;
+  const unsigned blocks = (unsigned)std::min<int64_t>((units + 255) / 256, 8192);
+  hipLaunchKernelGGL(pack_mx_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint16_t*>(scales),
+                     (uint32_t)rows, (uint32_t)n_chunks, (uint32_t)units, reinterpret_cast<uint16_t*>(dst));
+}
+
 // Transposed packed image: the rows of the image are the COLUMNS k of
 // x [rows, cols] (bf16) and its K dimension runs along x's rows, in the
 // layout pack_kernel writes (one 16 KiB block per (256-column tile, 32-row
@@ -1193,6 +1214,12 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows) {
     pl.ws_pack_offset[q] = off;
     off += align_up(pack_bytes[q], 256);
   }
+  // MX: packed E8M0 scale images of Wq and Hq (d/32 bytes per row)
+  const size_t mx_bytes[2] = {vrows * (size_t)(d / 32), trows * (size_t)(d / 32)};
+  for (int q = 0; q < 2; ++q) {
+    pl.ws_mx_offset[q] = off;
+    off += align_up(mx_bytes[q], 256);
+  }
   // full-vocabulary measures: the logits of both policies for one pass of
   // div_tiles token tiles, row-major with the padded vocabulary as stride
   pl.div_tiles = 0;
@@ -1254,8 +1281,10 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   pm.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[1]);
   pm.logit = reinterpret_cast<float*>(ws + pl.ws_logit_offset[1]);
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
-    pm.a_mx = static_cast<const uint8_t*>(dsc.wq_scales);
-    pm.b_mx = static_cast<const uint8_t*>(dsc.hq_scales);
+    launch_pack_mx(dsc.wq_scales, dsc.V, dsc.d, pl.n_vtiles, ws + pl.ws_mx_offset[0], s);
+    launch_pack_mx(dsc.hq_scales, dsc.n_rows, dsc.d, pl.n_ttiles, ws + pl.ws_mx_offset[1], s);
+    pm.a_mx = ws + pl.ws_mx_offset[0];
+    pm.b_mx = ws + pl.ws_mx_offset[1];
   } else {
     pm.a_scale = static_cast<const float*>(dsc.wq_scales);
     pm.b_scale = static_cast<const float*>(dsc.hq_scales);
@@ -1519,8 +1548,10 @@ hipError_t launch_sample(const acrl_sample_desc& dsc, const ScorePlan& pl, hipSt
   pm.best_id = reinterpret_cast<int32_t*>(ws + pl.ws_best_offset + 2 * best_plane);
   const unsigned grid = (unsigned)pl.grid;
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
-    pm.a_mx = static_cast<const uint8_t*>(dsc.wq_scales);
-    pm.b_mx = static_cast<const uint8_t*>(dsc.hq_scales);
+    launch_pack_mx(dsc.wq_scales, dsc.V, dsc.d, pl.n_vtiles, ws + pl.ws_mx_offset[0], s);
+    launch_pack_mx(dsc.hq_scales, dsc.n_rows, dsc.d, pl.n_ttiles, ws + pl.ws_mx_offset[1], s);
+    pm.a_mx = ws + pl.ws_mx_offset[0];
+    pm.b_mx = ws + pl.ws_mx_offset[1];
     launch_score_kernel<kMX, kEpiSample>(grid, pm, s);
   } else {
     pm.a_scale = static_cast<const float*>(dsc.wq_scales);
