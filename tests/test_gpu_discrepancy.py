@@ -71,6 +71,14 @@ def test_reduce_deterministic():
         assert np.array_equal(a[k], b[k]), k
 
 
+def _oracle_y(B, L, ng, mask, lp_pi, lp_mu, g):
+    """The discrepancy levels Y (and X) that both controllers take as inputs:
+    the oracle's reduce of the seeded batch, in the ABI's types."""
+    ref = oracle.discrepancy_reduce(B, L, lp_pi, lp_mu, mask, g, ng)
+    return {"seq_mean_d": ref["seq_mean_d"].astype(np.float32), "group_y": ref["group_y"].astype(np.float32),
+            "stats": ref["stats"].astype(np.float64), "seq_sum_logratio": ref["seq_sum_logratio"]}
+
+
 @pytest.mark.parametrize("level", [oracle.Y_GROUP, oracle.Y_SEQUENCE, oracle.Y_BATCH])
 @pytest.mark.parametrize("per_token", [False, True])
 def test_controller_matches_oracle(level, per_token):
@@ -78,7 +86,7 @@ def test_controller_matches_oracle(level, per_token):
     from paper_2607_24062_amd import acrl
     B, L, ng = 24, 300, 3
     mask, lp_pi, lp_mu, ent_pi, ent_mu, g = _batch(B, L, ng, 21)
-    red = _gpu_reduce(B, L, ng, mask, lp_pi, lp_mu, ent_pi, ent_mu, g)
+    red = _oracle_y(B, L, ng, mask, lp_pi, lp_mu, g)
     r = np.random.default_rng(22)
     adv = (r.normal(size=B * L if per_token else B)).astype(np.float32)
     adv[:3] = 0.0
@@ -109,7 +117,7 @@ def test_controller_modes_match_oracle(mode, k):
     from paper_2607_24062_amd import acrl
     B, L, ng = 24, 300, 3
     mask, lp_pi, lp_mu, ent_pi, ent_mu, g = _batch(B, L, ng, 31)
-    red = _gpu_reduce(B, L, ng, mask, lp_pi, lp_mu, ent_pi, ent_mu, g)
+    red = _oracle_y(B, L, ng, mask, lp_pi, lp_mu, g)
     adv = np.random.default_rng(32).normal(size=B).astype(np.float32)
     adv[:2] = 0.0
     t = lambda a: up(torch, dev, np.ascontiguousarray(a).reshape(-1))
