@@ -901,17 +901,21 @@ void launch_score_kernel(unsigned grid, const ScoreParams& p, hipStream_t s) {
 // 64-byte chunk of the rows, one 16 KiB block holding the tile's 256 row
 // pieces in row order, the four 16-byte columns of row r permuted to
 // positions c ^ ((r/4) % 4).  Rows past `rows` repeat the last row.  One
-// thread per 16 bytes: reads run along the source rows, writes land in
-// 64-byte runs.  `units` = n_tiles * 256 * (row_bytes / 16) < 2^32.
+// thread per 16 bytes; eight consecutive threads move one 128-byte line of a
+// source row (chunks 2p, 2p+1), so a wavefront reads 8 whole lines of 8
+// consecutive rows and writes two contiguous 512-byte runs (row_bytes is a
+// multiple of 128).  `units` = n_tiles * 256 * (row_bytes / 16) < 2^32.
 __global__ __launch_bounds__(256) void pack_kernel(const uint8_t* __restrict__ src, uint32_t rows,
                                                    uint32_t row_bytes, uint32_t units, uint8_t* __restrict__ dst) {
-  const uint32_t pieces = row_bytes / 16;
   const uint32_t n_chunks = row_bytes / kChunk;
+  const uint32_t n_pairs = n_chunks / 2;
   for (uint32_t u = blockIdx.x * blockDim.x + threadIdx.x; u < units; u += gridDim.x * blockDim.x) {
-    const uint32_t row = u / pieces;
-    const uint32_t piece = u - row * pieces;
+    const uint32_t c16 = u & 7, rest = u >> 3;
+    const uint32_t rr = rest % kTileV, tp = rest / kTileV;  // tp = tile * n_pairs + pair
+    const uint32_t tile = tp / n_pairs, pr = tp - tile * n_pairs;
+    const uint32_t piece = pr * 8 + c16;  // 16-byte piece of the source row
     const uint32_t kc = piece >> 2, c = piece & 3;
-    const uint32_t tile = row / kTileV, rr = row % kTileV;
+    const uint32_t row = tile * kTileV + rr;
     const uint32_t pos = c ^ ((rr >> 2) & 3);
     const uint32_t sr = row < rows ? row : rows - 1;
     const uint4 v = *reinterpret_cast<const uint4*>(src + (size_t)sr * row_bytes + piece * 16);
