@@ -198,3 +198,21 @@ def test_small_workload_end_to_end():
     wg = down(weight)
     # weight = exp(alpha * log-ratio): |dw| <= w * |alpha| * 2 * TOL_LOGP (+ Y differences)
     assert np.all(np.abs(wg - w_ref) <= wg * (0.65 * 3 * 2 * TOL_LOGP + 1e-3) + 1e-6)
+
+
+@pytest.mark.parametrize("B,L,ng", [(0, 16, 0), (0, 16, 3), (4, 16, 2), (3, 0, 2)])
+def test_reduce_empty_and_all_masked(B, L, ng):
+    # degenerate batches: no responses, no slots, or every slot masked
+    # (n_i = 0 everywhere): every output the oracle gives, zeros throughout
+    mask = np.zeros((B, L), np.uint8)
+    lp = np.log(np.full((B, L), 0.5)).astype(np.float32)
+    g = (np.arange(B) % max(ng, 1)).astype(np.int32)
+    got = _gpu_reduce(B, L, ng, mask, lp, lp - 0.1, lp * 0, lp * 0, g)
+    ref = oracle.discrepancy_reduce(B, L, lp, lp - 0.1, mask, g, ng)
+    assert np.array_equal(got["seq_len"], ref["seq_len"])
+    assert np.array_equal(got["stats"], ref["stats"])
+    assert np.array_equal(got["group_y"], ref["group_y"].astype(np.float32))
+    assert np.array_equal(got["seq_mean_d"], ref["seq_mean_d"].astype(np.float32))
+    assert np.array_equal(got["group_nseq"], ref["group_nseq"])
+    if B * L:
+        assert np.all(got["d_tok"] == 0)
