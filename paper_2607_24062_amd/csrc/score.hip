@@ -9,13 +9,16 @@
 //    block holds token column l%32 and 16 vocabulary rows.  The softmax
 //    statistics of a token are then reduced inside each lane across all the
 //    vocabulary rows it sees; lanes and waves are merged once per workgroup.
-//  * Workgroup tile: 256 vocabulary rows x 256 tokens, 4 waves (2 x 2), each
-//    wave 128 x 128 = 4 x 4 MFMA 32x32 blocks (256 fp32 accumulators / lane).
+//  * Workgroup tile: 256 vocabulary rows x 256 tokens, one workgroup per CU,
+//    4 waves of 128 x 128 (256 accumulators per lane) or 8 waves of 128 x 64
+//    (128 accumulators, two waves per SIMD), chosen per instantiation.
 //    BF16: v_mfma_f32_32x32x16_bf16.  FP8: v_mfma_f32_32x32x64_f8f6f4.
 //    MXFP8: v_mfma_scale_f32_32x32x64_f8f6f4 with per-lane E8M0 block scales.
-//  * K is streamed in 128-byte chunks per row (64 bf16 or 128 fp8 values),
-//    double-buffered in LDS (2 x 64 KiB) with an XOR swizzle of the 16-byte
-//    columns so that fragment reads are bank-conflict free.
+//  * K is streamed in 64-byte chunks per row (32 bf16 or 64 fp8 values) from
+//    packed tile images straight into LDS (buffer_load ... lds), in a ring of
+//    5 stages (4 for the per-row and MX scorers) with one barrier per chunk
+//    and an XOR swizzle of the 16-byte columns so that fragment reads are
+//    bank-conflict free.
 //  * Each workgroup sweeps a strip of vocabulary tiles for one token tile and
 //    keeps a running (max, sum, entropy-sum) state per token in registers:
 //    the [rows, V] logits never reach memory.  Online update, in log2 units
@@ -247,6 +250,10 @@ void score_kernel(ScoreParams p) {
   constexpr bool SOFTMAX = EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ;
   static_assert(MODE == kBF16 || SOFTMAX, "the backward epilogues take bf16 operands");
   constexpr int NS = Pipe<MODE>::kStages;
+  // FP8 per-tensor / MX scorers start each tile's accumulators with an
+  // inline-zero MFMA instead of clearing them after the epilogue (measured:
+  // faster there; the BF16 and per-row FP8 kernels keep the clearing)
+  constexpr bool kZeroStart = SOFTMAX && (MODE == kFP8Tensor || MODE == kMX);
   constexpr int SB = Pipe<MODE>::kScaleBytes;
   constexpr int LPC = Pipe<MODE>::template loads_per_chunk<NW>();
   constexpr int RSB = Pipe<MODE>::kRowScaleBytes;
@@ -434,20 +441,22 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
     for (int j = 0; j < JT; ++j) sb[j] = scales_at(stg)[(kTileV + wt * TW + j * 32 + r32) * 2 + g];
   };
-  auto mfma_group = [&](int grp, const FragT& fa, const FragT (&fb)[JT], int sa, const int (&sb)[JT]) {
+  // zc: the accumulators start from zero (the first K step of a tile), so
+  // the MFMA takes an inline zero instead of them and no clearing is needed
+  auto mfma_group = [&](auto zc_tag, int grp, const FragT& fa, const FragT (&fb)[JT], int sa, const int (&sb)[JT]) {
+    constexpr bool kZero = decltype(zc_tag)::value;
     const int bb = grp & 3;
 #pragma unroll
     for (int j = 0; j < JT; ++j) {
+      const f32x16 c = kZero ? f32x16{} : acc[bb][j];
       if constexpr (MODE == kBF16) {
-        acc[bb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb[j], acc[bb][j], 0, 0, 0);
+        acc[bb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb[j], c, 0, 0, 0);
       } else if constexpr (MODE == kMX) {
-        acc[bb][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], acc[bb][j], 0, 0, 0,
-                                                                    sa, 0, sb[j]);
+        acc[bb][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], c, 0, 0, 0, sa, 0, sb[j]);
       } else {
         (void)sa;
         (void)sb;
-        acc[bb][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], acc[bb][j], 0, 0, 0,
-                                                                    0, 0, 0);
+        acc[bb][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], c, 0, 0, 0, 0, 0, 0);
       }
     }
   };
@@ -745,8 +754,11 @@ void score_kernel(ScoreParams p) {
     return n;
   };
   int stg = 0;  // stage of the current chunk
-  auto chunk = [&](auto steady_tag, int it, Frags& cur, Frags& nxt) {
+  // first_tag: the tile's first chunk, whose first K step starts the
+  // accumulators from zero
+  auto chunk = [&](auto steady_tag, auto first_tag, int it, Frags& cur, Frags& nxt) {
     constexpr bool kSteady = decltype(steady_tag)::value;
+    constexpr bool kFirst = decltype(first_tag)::value;
     const bool has_next = kSteady || it + 1 < n_iter;
     const int nst = stg + 1 == NS ? 0 : stg + 1;
     FragT af[G];       // A of this chunk's groups
@@ -785,7 +797,8 @@ void score_kernel(ScoreParams p) {
           if constexpr (MODE == kMX) read_sb(nst, nxt.sb);
         }
       }
-      mfma_group(k, af[k], bf[k / 4], sa[k], cur.sb);
+      if (kFirst && k < 4) mfma_group(std::true_type{}, k, af[k], bf[k / 4], sa[k], cur.sb);
+      else mfma_group(std::false_type{}, k, af[k], bf[k / 4], sa[k], cur.sb);
       if constexpr (kSteady) {
         // keep this group's LDS reads ahead of its MFMAs (the scheduler
         // would otherwise sink each read to just before its use)
@@ -802,21 +815,36 @@ void score_kernel(ScoreParams p) {
     // while requests remain, and wait for every load
     const int kc_steady = min(p.n_chunks, max(0, n_iter - NS - it));
     int kc = 0;
+    if constexpr (kZeroStart) {
+    // the first pair (every tile has an even number >= 2 of chunks): its
+    // first chunk starts the accumulators from an inline zero
+    if (kc_steady >= 2) {
+      chunk(std::true_type{}, std::true_type{}, it, f0, f1);
+      chunk(std::true_type{}, std::false_type{}, it + 1, f1, f0);
+    } else {
+      chunk(std::false_type{}, std::true_type{}, it, f0, f1);
+      chunk(std::false_type{}, std::false_type{}, it + 1, f1, f0);
+    }
+    kc = 2;
+    it += 2;
+    }
     for (; kc + 1 < kc_steady; kc += 2, it += 2) {
-      chunk(std::true_type{}, it, f0, f1);
-      chunk(std::true_type{}, it + 1, f1, f0);
+      chunk(std::true_type{}, std::false_type{}, it, f0, f1);
+      chunk(std::true_type{}, std::false_type{}, it + 1, f1, f0);
     }
     for (; kc < p.n_chunks; kc += 2, it += 2) {
-      chunk(std::false_type{}, it, f0, f1);
-      chunk(std::false_type{}, it + 1, f1, f0);
+      chunk(std::false_type{}, std::false_type{}, it, f0, f1);
+      chunk(std::false_type{}, std::false_type{}, it + 1, f1, f0);
     }
     if constexpr (SOFTMAX) epilogue(vt_begin + q, q);
     else if constexpr (EPI == kEpiGrad) grad_epilogue(vt_begin + q);
     else store_epilogue(vt_begin + q);
+    if constexpr (!kZeroStart) {
 #pragma unroll
-    for (int b = 0; b < 4; ++b)
+      for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int j = 0; j < JT; ++j) acc[b][j] = f32x16{};
+        for (int j = 0; j < JT; ++j) acc[b][j] = f32x16{};
+    }
   }
   if constexpr (!SOFTMAX) return;
   __syncthreads();  // every wave is done with the stages before LDS is reused
