@@ -494,17 +494,19 @@ void score_kernel(ScoreParams p) {
       constexpr bool kTail = decltype(tail_tag)::value;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
-        float rs[16];
-        if constexpr (MODE == kFP8Row) {
-          const float* rsl = rowscales_at(q) + wv * 128 + b * 32 + 4 * g;
-#pragma unroll
-          for (int qq = 0; qq < 4; ++qq) {
-            const f32x4 f = *reinterpret_cast<const f32x4*>(rsl + 8 * qq);
-            rs[4 * qq + 0] = f[0]; rs[4 * qq + 1] = f[1]; rs[4 * qq + 2] = f[2]; rs[4 * qq + 3] = f[3];
-          }
-        }
 #pragma unroll
         for (int j = 0; j < JT; ++j) {
+          float rs[16];
+          if constexpr (MODE == kFP8Row) {
+            // the block's 16 weight-row scales, read per token block (fewer
+            // live registers than keeping them across the token blocks)
+            const float* rsl = rowscales_at(q) + wv * 128 + b * 32 + 4 * g;
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+              const f32x4 f = *reinterpret_cast<const f32x4*>(rsl + 8 * qq);
+              rs[4 * qq + 0] = f[0]; rs[4 * qq + 1] = f[1]; rs[4 * qq + 2] = f[2]; rs[4 * qq + 3] = f[3];
+            }
+          }
           float v[16];
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
@@ -910,11 +912,12 @@ void score_kernel(ScoreParams p) {
 }
 
 // Waves per workgroup of each instantiation (measured on the MI355X): two
-// per SIMD where the variant fits its registers without spilling and runs
-// faster; one per SIMD otherwise.
+// per SIMD where the variant runs faster that way (the per-row FP8 scorer
+// spills 40 bytes per lane at 8 waves and is still 5-7 % faster); one per
+// SIMD otherwise.
 template <int MODE, int EPI>
 constexpr int waves_for() {
-  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor)) || (EPI == kEpiSoftmaxZ && MODE == kBF16))
+  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) || (EPI == kEpiSoftmaxZ && MODE == kBF16))
              ? 8
              : 4;
 }
