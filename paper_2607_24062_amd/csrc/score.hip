@@ -590,12 +590,16 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
               for (int ii = 0; ii < 4; ++ii) {
                 const int i = 4 * q4 + ii;
+                // the logit again from its accumulator (scaled as above):
+                // fewer values live across the generator calls
+                float vi = acc_read(acc[b][j][i]);
+                if constexpr (MODE == kFP8Row) vi *= rs[i];
                 const float u = ((float)(w4[ii] >> 9) + 0.5f) * 0x1p-23f;
-                float key = fmaf(v[i], c2[j], -__builtin_amdgcn_logf(-__builtin_amdgcn_logf(u)));
+                float key = fmaf(vi, c2[j], -__builtin_amdgcn_logf(-__builtin_amdgcn_logf(u)));
                 if constexpr (kTail) key = (nv - (float)(16 * b + i)) > 0.0f ? key : -INFINITY;
                 if (key > bk[j]) {
                   bk[j] = key;
-                  bz[j] = v[i] * cz[j];
+                  bz[j] = vi * cz[j];
                   bi[j] = vb + ii;
                 }
               }
@@ -913,11 +917,13 @@ void score_kernel(ScoreParams p) {
 
 // Waves per workgroup of each instantiation (measured on the MI355X): two
 // per SIMD where the variant runs faster that way (the per-row FP8 scorer
-// spills 40 bytes per lane at 8 waves and is still 5-7 % faster); one per
-// SIMD otherwise.
+// spills 40 bytes per lane at 8 waves and is still 5-7 % faster; the
+// sampling variants spill at either width, far less at 8, and run ~20 %
+// faster there); one per SIMD otherwise.
 template <int MODE, int EPI>
 constexpr int waves_for() {
-  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) || (EPI == kEpiSoftmaxZ && MODE == kBF16))
+  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) || (EPI == kEpiSoftmaxZ && MODE == kBF16) ||
+          (EPI == kEpiSample && MODE != kMX))
              ? 8
              : 4;
 }
