@@ -147,8 +147,9 @@ acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, vo
  * for rows = V and rows = n_rows: (rows rounded up to 256) * d / 8 < 2^32;
  * token ids in [0, V) (else the row's outputs are NaN and *error_flag, if
  * given, becomes nonzero; the flag is never cleared by the library).
- * The workspace holds a tiled copy of W, h, Wq and hq (about 3 (V + n_rows) d
- * bytes) besides the per-strip partial states.
+ * The workspace holds a tiled copy of W, h, Wq and hq and of the E8M0 scales
+ * of Wq and hq (about (3 + 1/32) (V + n_rows) d bytes) besides the per-strip
+ * partial states.
  *
  * Full-vocabulary measures (optional; the paper's measure is the absolute
  * distance on the sampled token, Eq. distance_metric, and it names the KL
