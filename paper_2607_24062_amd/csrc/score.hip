@@ -201,8 +201,32 @@ __device__ __forceinline__ void sched_ds_reads(int n) {
     case 3: __builtin_amdgcn_sched_group_barrier(0x100, 3, 0); break;
     case 5: __builtin_amdgcn_sched_group_barrier(0x100, 5, 0); break;
     case 10: __builtin_amdgcn_sched_group_barrier(0x100, 10, 0); break;
+    case 12: __builtin_amdgcn_sched_group_barrier(0x100, 12, 0); break;
     case 15: __builtin_amdgcn_sched_group_barrier(0x100, 15, 0); break;
     default: break;
+  }
+}
+
+// MXFP8 product whose E8M0 scales are byte oa of sa (A rows) and byte ob of
+// sb (B rows).  The byte selects are immediates of the instruction; oa and ob
+// are constants once the caller's loops are unrolled.
+template <int OA>
+__device__ __forceinline__ f32x16 mfma_mx_b(const i32x8& a, const i32x8& b, const f32x16& c, int sa, int sb,
+                                            int ob) {
+  switch (ob) {
+    case 0: return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, OA, sa, 0, sb);
+    case 1: return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, OA, sa, 1, sb);
+    case 2: return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, OA, sa, 2, sb);
+    default: return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, OA, sa, 3, sb);
+  }
+}
+__device__ __forceinline__ f32x16 mfma_mx(const i32x8& a, const i32x8& b, const f32x16& c, int sa, int oa, int sb,
+                                          int ob) {
+  switch (oa) {
+    case 0: return mfma_mx_b<0>(a, b, c, sa, sb, ob);
+    case 1: return mfma_mx_b<1>(a, b, c, sa, sb, ob);
+    case 2: return mfma_mx_b<2>(a, b, c, sa, sb, ob);
+    default: return mfma_mx_b<3>(a, b, c, sa, sb, ob);
   }
 }
 
@@ -432,18 +456,19 @@ void score_kernel(ScoreParams p) {
       else bf[j] = read16x2(row);
     }
   };
-  // MX scales of the chunk in stage stg: 2 bytes per row (W rows, then H
-  // rows); lane group g takes block 2kc + g.
-  auto read_sa = [&](int stg, int grp) -> int {
-    return scales_at(stg)[(wv * 128 + (grp & 3) * 32 + r32) * 2 + g];
+  // MX scales of the chunk in stage stg (512 bytes of W rows, then 512 of H
+  // rows, in the order pack_mx_kernel writes): one dword per lane and
+  // operand holds the block-2kc+g scales of the lane's row in each of the
+  // wave's four 32-row blocks, byte b for block b.
+  auto read_sa = [&](int stg) -> int {
+    return *reinterpret_cast<const int*>(scales_at(stg) + ((wv * 2 + g) * 32 + r32) * 4);
   };
-  auto read_sb = [&](int stg, int (&sb)[JT]) {
-#pragma unroll
-    for (int j = 0; j < JT; ++j) sb[j] = scales_at(stg)[(kTileV + wt * TW + j * 32 + r32) * 2 + g];
+  auto read_sb = [&](int stg) -> int {
+    return *reinterpret_cast<const int*>(scales_at(stg) + 2 * kTileV + ((wt * 2 + g) * 32 + r32) * 4);
   };
   // zc: the accumulators start from zero (the first K step of a tile), so
   // the MFMA takes an inline zero instead of them and no clearing is needed
-  auto mfma_group = [&](auto zc_tag, int grp, const FragT& fa, const FragT (&fb)[JT], int sa, const int (&sb)[JT]) {
+  auto mfma_group = [&](auto zc_tag, int grp, const FragT& fa, const FragT (&fb)[JT], int sa, int sb) {
     constexpr bool kZero = decltype(zc_tag)::value;
     const int bb = grp & 3;
 #pragma unroll
@@ -452,7 +477,7 @@ void score_kernel(ScoreParams p) {
       if constexpr (MODE == kBF16) {
         acc[bb][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb[j], c, 0, 0, 0);
       } else if constexpr (MODE == kMX) {
-        acc[bb][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(fa, fb[j], c, 0, 0, 0, sa, 0, sb[j]);
+        acc[bb][j] = mfma_mx(fa, fb[j], c, sa, bb, sb, j);
       } else {
         (void)sa;
         (void)sb;
@@ -737,26 +762,24 @@ void score_kernel(ScoreParams p) {
   // straight into the registers it will use.
   struct Frags {
     FragT a[L], b[JT];
-    int sa[L], sb[JT];
+    int sa, sb;  // MX: the chunk's scale dwords of the W and H rows
   };
   Frags f0, f1;
 #pragma unroll
-  for (int l = 0; l < L; ++l) {
-    f0.a[l] = read_a(0, l);
-    f0.sa[l] = 0;
-    if constexpr (MODE == kMX) f0.sa[l] = read_sa(0, l);
-  }
+  for (int l = 0; l < L; ++l) f0.a[l] = read_a(0, l);
   read_b(0, 0, f0.b);
-#pragma unroll
-  for (int j = 0; j < JT; ++j) f0.sb[j] = 0;
-  if constexpr (MODE == kMX) read_sb(0, f0.sb);
+  f0.sa = f0.sb = f1.sa = f1.sb = 0;
+  if constexpr (MODE == kMX) {
+    f0.sa = read_sa(0);
+    f0.sb = read_sb(0);
+  }
 
   // LDS read instructions issued in group k (for group k + L)
   auto reads_at = [](int k) constexpr {
     const int t = k + L, tt = t % G;
     constexpr int per_frag = (MODE == kBF16) ? 1 : 2;
-    int n = per_frag + (MODE == kMX ? 1 : 0);                               // A (+ its MX scale)
-    if (tt % 4 == 0) n += JT * per_frag + (MODE == kMX && tt == 0 ? JT : 0);  // B of a new step
+    int n = per_frag;                                                      // A
+    if (tt % 4 == 0) n += JT * per_frag + (MODE == kMX && tt == 0 ? 2 : 0);  // B of a new step (+ MX scales)
     return n;
   };
   int stg = 0;  // stage of the current chunk
@@ -769,12 +792,8 @@ void score_kernel(ScoreParams p) {
     const int nst = stg + 1 == NS ? 0 : stg + 1;
     FragT af[G];       // A of this chunk's groups
     FragT bf[2][JT];    // B of this chunk's K steps (BF16: 2, FP8: 1)
-    int sa[G];
 #pragma unroll
-    for (int l = 0; l < L; ++l) {
-      af[l] = cur.a[l];
-      sa[l] = cur.sa[l];
-    }
+    for (int l = 0; l < L; ++l) af[l] = cur.a[l];
 #pragma unroll
     for (int j = 0; j < JT; ++j) bf[0][j] = cur.b[j];
 #pragma unroll
@@ -791,20 +810,19 @@ void score_kernel(ScoreParams p) {
       }
       if (t < G) {
         af[t] = read_a(stg, t);
-        sa[t] = 0;
-        if constexpr (MODE == kMX) sa[t] = read_sa(stg, t);
         if (t % 4 == 0) read_b(stg, t, bf[t / 4]);  // BF16: second K step
       } else if (has_next) {
         nxt.a[t - G] = read_a(nst, t - G);
-        nxt.sa[t - G] = 0;
-        if constexpr (MODE == kMX) nxt.sa[t - G] = read_sa(nst, t - G);
         if (t == G) {
           read_b(nst, 0, nxt.b);
-          if constexpr (MODE == kMX) read_sb(nst, nxt.sb);
+          if constexpr (MODE == kMX) {
+            nxt.sa = read_sa(nst);
+            nxt.sb = read_sb(nst);
+          }
         }
       }
-      if (kFirst && k < 4) mfma_group(std::true_type{}, k, af[k], bf[k / 4], sa[k], cur.sb);
-      else mfma_group(std::false_type{}, k, af[k], bf[k / 4], sa[k], cur.sb);
+      if (kFirst && k < 4) mfma_group(std::true_type{}, k, af[k], bf[k / 4], cur.sa, cur.sb);
+      else mfma_group(std::false_type{}, k, af[k], bf[k / 4], cur.sa, cur.sb);
       if constexpr (kSteady) {
         // keep this group's LDS reads ahead of its MFMAs (the scheduler
         // would otherwise sink each read to just before its use)
@@ -961,28 +979,36 @@ __global__ __launch_bounds__(256) void pack_kernel(const uint8_t* __restrict__ s
 }
 
 // Packed MX scale image read by score_kernel: for each 256-row tile and each
-// 64-byte chunk kc, the E8M0 scales of MX blocks 2kc, 2kc+1 of the tile's
-// 256 rows in row order (2 bytes per row, 512 bytes).  Rows past `rows`
-// repeat the last row.  One thread per row and chunk; `units` = n_tiles *
-// 256 * n_chunks < 2^32.
-__global__ __launch_bounds__(256) void pack_mx_kernel(const uint16_t* __restrict__ src, uint32_t rows,
-                                                      uint32_t n_chunks, uint32_t units, uint16_t* __restrict__ dst) {
+// 64-byte chunk kc, 128 dwords holding the E8M0 scales of MX blocks 2kc,
+// 2kc+1 of the tile's 256 rows (512 bytes).  Dword (h, g, r) = (2h + g) * 32
+// + r carries block 2kc + g of rows 128h + 32b + r in its bytes b = 0..3: the
+// dword one lane of a 128-row wave half needs for its four 32-row blocks.
+// Rows past `rows` repeat the last row.  One thread per dword; `units` =
+// n_tiles * n_chunks * 128 < 2^32.
+__global__ __launch_bounds__(256) void pack_mx_kernel(const uint8_t* __restrict__ src, uint32_t rows,
+                                                      uint32_t n_chunks, uint32_t units, uint32_t* __restrict__ dst) {
+  const uint32_t row_bytes = 2 * n_chunks;  // d / 32 scale bytes per row
   for (uint32_t u = blockIdx.x * blockDim.x + threadIdx.x; u < units; u += gridDim.x * blockDim.x) {
-    const uint32_t rr = u % kTileV, tc = u / kTileV;  // tc = tile * n_chunks + kc
+    const uint32_t r = u & 31, g = (u >> 5) & 1, h = (u >> 6) & 1, tc = u >> 7;  // tc = tile * n_chunks + kc
     const uint32_t tile = tc / n_chunks, kc = tc - tile * n_chunks;
-    const uint32_t row = tile * kTileV + rr;
-    const uint32_t sr = row < rows ? row : rows - 1;
-    dst[u] = src[(size_t)sr * n_chunks + kc];
+    uint32_t word = 0;
+#pragma unroll
+    for (uint32_t b = 0; b < 4; ++b) {
+      const uint32_t row = tile * kTileV + h * 128 + b * 32 + r;
+      const uint32_t sr = row < rows ? row : rows - 1;
+      word |= (uint32_t)src[(size_t)sr * row_bytes + 2 * kc + g] << (8 * b);
+    }
+    dst[u] = word;
   }
 }
 
 inline void launch_pack_mx(const void* scales, int64_t rows, int64_t d, int64_t n_tiles, uint8_t* dst,
                            hipStream_t s) {
   const int64_t n_chunks = d / kChunk;  // a row holds d / 32 scale bytes = 2 per chunk
-  const int64_t units = n_tiles * kTileV * n_chunks;
+  const int64_t units = n_tiles * n_chunks * 128;  // one dword per 4 rows and MX block
   const unsigned blocks = (unsigned)std::min<int64_t>((units + 255) / 256, 8192);
-  hipLaunchKernelGGL(pack_mx_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint16_t*>(scales),
-                     (uint32_t)rows, (uint32_t)n_chunks, (uint32_t)units, reinterpret_cast<uint16_t*>(dst));
+  hipLaunchKernelGGL(pack_mx_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint8_t*>(scales),
+                     (uint32_t)rows, (uint32_t)n_chunks, (uint32_t)units, reinterpret_cast<uint32_t*>(dst));
 }
 
 // Transposed packed image: the rows of the image are the COLUMNS k of
