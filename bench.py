@@ -47,6 +47,8 @@ def main():
                     help="skip the full-vocabulary KL / Euclidean leg")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the surrogate + LM-head backward leg")
+    ap.add_argument("--no-library", action="store_true",
+                    help="skip the vendor-library GEMM leg (hipBLASLt through torch, no softmax)")
     ap.add_argument("--counters", action="store_true",
                     help="copy calibration + one step only (for rocprofv3 --pmc passes)")
     args = ap.parse_args()
@@ -275,10 +277,72 @@ def main():
         line["backward"] = backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv,
                                         X_ref[0])
 
+    if not args.no_library:
+        line["library_gemm"] = library_leg(torch, w, T, H, W, hq, hs, wq, ws, t_pi, t_mu)
+
     # ---------------- CPU baseline: the oracle on host cores, bounded sample
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, T, H, W, args.cpu_seconds)
     print(json.dumps(line), flush=True)
+
+
+def library_leg(torch, w, T, H, W, hq, hs, wq, ws, pi_ms, mu_ms, reps=2):
+    """Context for the scorers' rates, not part of the path: the vendor
+    library (hipBLASLt through torch) on the same two contractions with no
+    softmax, logits = H W^T with bf16 output, in BF16 and (per-tensor
+    scaling only) as the scaled FP8 product of the same quantized operands.
+    Chunks of 32768 tokens keep the [T, V] logits it writes in HBM; the
+    token count is cut to a multiple of 16 for the FP8 product."""
+    d, V = w.d, w.V
+    CH = 32768
+    Tm = (T // 16) * 16
+    chunks = [(s0, min(CH, Tm - s0)) for s0 in range(0, Tm, CH)]
+    flops = 2.0 * Tm * V * d
+    out = torch.empty((CH, V), dtype=torch.bfloat16, device=H.device)
+    res = {"what": "torch.mm (hipBLASLt) logits = H W^T, bf16 out, and torch._scaled_mm on the FP8 operands; "
+                   "no softmax; %d chunks of <= %d tokens" % (len(chunks), CH),
+           "tokens": Tm, "flops": flops}
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    def bf16():
+        for s0, n in chunks:
+            torch.mm(H[s0:s0 + n], W.t(), out=out[:n])
+
+    ms = timed(bf16)
+    tf = flops / (ms * 1e-3) / 1e12
+    res["bf16"] = {"ms": round(ms, 3), "TFLOPs": round(tf, 1), "frac_of_peak": round(tf / 2500.0, 4),
+                   "fused_pi_rate_over_library": round((T / float(pi_ms)) / (Tm / ms), 4)}
+    log("library bf16: %.2f ms, %.0f TFLOP/s" % (ms, tf))
+    if w.scaling == inputs.PER_TENSOR:
+        try:
+            f8 = torch.float8_e4m3fn
+            hq8, wq8 = hq.view(f8), wq.view(f8)
+
+            def fp8():
+                for s0, n in chunks:
+                    torch._scaled_mm(hq8[s0:s0 + n], wq8.t(), scale_a=hs, scale_b=ws,
+                                     out_dtype=torch.bfloat16)
+
+            ms = timed(fp8)
+            tf = flops / (ms * 1e-3) / 1e12
+            res["fp8"] = {"ms": round(ms, 3), "TFLOPs": round(tf, 1), "frac_of_peak": round(tf / 5000.0, 4),
+                          "fused_mu_rate_over_library": round((T / float(mu_ms)) / (Tm / ms), 4)}
+            log("library fp8: %.2f ms, %.0f TFLOP/s" % (ms, tf))
+        except (RuntimeError, TypeError) as e:
+            res["fp8"] = {"error": str(e)[:200]}
+    del out
+    torch.cuda.empty_cache()
+    return res
 
 
 def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, score_ms, reps=2):
