@@ -158,6 +158,8 @@ def main():
             divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, 0.0, reps=0)
         if not args.no_backward:
             backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv, 1.0, reps=0)
+        if not args.no_library:
+            library_leg(torch, w, T, H, W, hq, hs, wq, ws, 1.0, 1.0, reps=0)
         torch.cuda.synchronize()
         log("counters run done")
         return
@@ -306,6 +308,8 @@ def library_leg(torch, w, T, H, W, hq, hs, wq, ws, pi_ms, mu_ms, reps=2):
     def timed(fn):
         fn()
         torch.cuda.synchronize()
+        if reps == 0:  # one untimed pass (counter collection)
+            return 1.0
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record()
         for _ in range(reps):
@@ -342,7 +346,7 @@ def library_leg(torch, w, T, H, W, hq, hs, wq, ws, pi_ms, mu_ms, reps=2):
             res["fp8"] = {"error": str(e)[:200]}
     del out
     torch.cuda.empty_cache()
-    return res
+    return res if reps else None
 
 
 def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, score_ms, reps=2):
@@ -480,6 +484,17 @@ def hbm_kernels(torch, acrl, dev, H, w, reps=5):
                                "frac_of_8TBps": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4),
                                "bytes": int(nbytes)}
     del lp_pi, lp_mu, ent, mask
+    # what a plain device copy reaches on this GPU (context for the figures
+    # above): torch's copy (the runtime's blit kernel) and an elementwise
+    # kernel, 1 GiB read + 1 GiB written each
+    src = torch.ones(1 << 29, dtype=torch.bfloat16, device=dev)
+    dst = torch.empty_like(src)
+    for name, fn in (("copy_1GiB", lambda: dst.copy_(src)), ("elementwise_neg_1GiB", lambda: torch.neg(src, out=dst))):
+        ms = timed(fn)
+        nbytes = 2.0 * (1 << 30)
+        res[name] = {"ms": round(ms, 4), "GBps": round(nbytes / ms / 1e6, 1),
+                     "frac_of_8TBps": round(nbytes / ms / 1e6 / PEAK_HBM_GBS, 4), "bytes": int(nbytes)}
+    del src, dst
     torch.cuda.empty_cache()
     log("HBM kernels:", res)
     return res

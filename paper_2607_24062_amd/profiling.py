@@ -129,7 +129,46 @@ def load_traffic(md_path: str):
     return t
 
 
+def mfma_markdown(counter_csv: str, trace_csv: str, title: str, commands: str) -> str:
+    """Shader clock and matrix-core busy share per kernel, from one
+    `--pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE` pass and a kernel trace
+    of the same command.  GRBM_GUI_ACTIVE reads the sum over the 8 XCDs, so
+    clock = GUI_ACTIVE / 8 / duration; busy = MFMA_BUSY / (GUI_ACTIVE / 8 x
+    1024 SIMDs); busy x clock / 2.4 GHz is the share of the MFMA peak."""
+    cnt = {}
+    with open(counter_csv) as f:
+        for r in csv.DictReader(f):
+            d = cnt.setdefault(short_name(r["Kernel_Name"]), {})
+            d.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    dur = {}
+    with open(trace_csv) as f:
+        for r in csv.DictReader(f):
+            dur.setdefault(short_name(r["Kernel_Name"]), []).append(
+                (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    lines = ["# " + title, "", "Commands (from the repository root on one MI355X):", "", "```", commands, "```", "",
+             "| kernel | dispatches | mean ms | clock GHz | MFMA busy | busy x clock / 2.4 GHz |",
+             "|---|---|---|---|---|---|"]
+    rows = []
+    for k, d in cnt.items():
+        if "GRBM_GUI_ACTIVE" not in d or "SQ_VALU_MFMA_BUSY_CYCLES" not in d or k not in dur:
+            continue
+        g = sum(d["GRBM_GUI_ACTIVE"]) / len(d["GRBM_GUI_ACTIVE"]) / 8.0
+        m = sum(d["SQ_VALU_MFMA_BUSY_CYCLES"]) / len(d["SQ_VALU_MFMA_BUSY_CYCLES"])
+        t = sum(dur[k]) / len(dur[k])
+        if m <= 0 or t < 1e-3:
+            continue
+        clk = g / t / 1e9
+        busy = m / (g * 1024.0)
+        rows.append((t, "| %s | %d | %.2f | %.3f | %.1f%% | %.1f%% |" % (
+            k, len(d["GRBM_GUI_ACTIVE"]), t * 1e3, clk, 100 * busy, 100 * busy * clk / 2.4)))
+    lines += [r for _, r in sorted(rows, reverse=True)]
+    return "\n".join(lines) + "\n"
+
+
 def main(argv):
+    if len(argv) >= 5 and argv[0] == "mfma":
+        sys.stdout.write(mfma_markdown(argv[1], argv[2], argv[3], argv[4]))
+        return 0
     if len(argv) >= 4 and argv[0] == "stats":
         sys.stdout.write(stats_markdown(argv[1], argv[2], argv[3]))
     elif len(argv) >= 5 and argv[0] == "traffic":
