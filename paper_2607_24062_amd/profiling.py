@@ -165,7 +165,37 @@ def mfma_markdown(counter_csv: str, trace_csv: str, title: str, commands: str) -
     return "\n".join(lines) + "\n"
 
 
+def per_cu_markdown(counter_csv: str, title: str, command: str) -> str:
+    """Per-kernel means of every counter of one `--pmc` pass, as events per
+    CU-cycle: value / (GRBM_GUI_ACTIVE / 8 x 256 CUs); the pass must hold
+    GRBM_GUI_ACTIVE."""
+    cnt = {}
+    with open(counter_csv) as f:
+        for r in csv.DictReader(f):
+            d = cnt.setdefault(short_name(r["Kernel_Name"]), {})
+            d.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    names = sorted({c for d in cnt.values() for c in d if c != "GRBM_GUI_ACTIVE"})
+    lines = ["# " + title, "", "Command (from the repository root on one MI355X):", "", "```", command, "```", "",
+             "Values per CU-cycle (counter / (GRBM_GUI_ACTIVE / 8 x 256)).", "",
+             "| kernel | GUI_ACTIVE / 8 | " + " | ".join(names) + " |",
+             "|---|---|" + "---|" * len(names)]
+    rows = []
+    for k, d in cnt.items():
+        if "GRBM_GUI_ACTIVE" not in d:
+            continue
+        g = sum(d["GRBM_GUI_ACTIVE"]) / len(d["GRBM_GUI_ACTIVE"]) / 8.0
+        if g < 1e6:
+            continue
+        cells = ["%.4f" % (sum(d[c]) / len(d[c]) / (g * 256.0)) if c in d else "" for c in names]
+        rows.append((g, "| %s | %.3e | %s |" % (k, g, " | ".join(cells))))
+    lines += [r for _, r in sorted(rows, reverse=True)]
+    return "\n".join(lines) + "\n"
+
+
 def main(argv):
+    if len(argv) >= 4 and argv[0] == "percu":
+        sys.stdout.write(per_cu_markdown(argv[1], argv[2], argv[3]))
+        return 0
     if len(argv) >= 5 and argv[0] == "mfma":
         sys.stdout.write(mfma_markdown(argv[1], argv[2], argv[3], argv[4]))
         return 0
