@@ -1233,15 +1233,22 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows) {
   pl.n_vtiles = (int)((V + kTileV - 1) / kTileV);
   pl.n_tblocks = (pl.n_ttiles + kBlockT - 1) / kBlockT;
   // Strips: a multiple of kBlockS (or every tile its own strip when there
-  // are fewer tiles).  One workgroup per CU (256 CUs): minimise the makespan
-  // ceil(grid / 256) * (tiles-per-strip + 1/2), the half tile standing for a
-  // workgroup's fixed cost (prologue, state merge, partial writes); ties ->
-  // fewer strips.
+  // are fewer tiles), at most kMaxTilesPerStrip tiles each.  One workgroup
+  // per CU (256 CUs): minimise the makespan ceil(grid / 256) *
+  // (tiles-per-strip + 1/2), the half tile standing for a workgroup's fixed
+  // cost (prologue, state merge, partial writes); ties -> fewer strips.  The
+  // cap bounds a workgroup's duration: workgroup times differ by up to ~7 %
+  // between XCDs and CUs, and the last workgroups of a CU end spread over
+  // about one workgroup time (measured on the MI355X: 75-tile strips at
+  // d = 4096 take ~8 ms and left ~4 % of the CU time idle; 15-19-tile
+  // strips ran the pi and mu kernels 2-3 % faster).
+  constexpr int kMaxTilesPerStrip = 20;
   const int64_t cus = 256;
   int best_s = 0;
   int64_t best_cost = -1;
   auto consider = [&](int s) {
     const int tps = (pl.n_vtiles + s - 1) / s;
+    if (tps > kMaxTilesPerStrip) return;  // always reachable: s = n_vtiles gives 1 or 2
     const int strips = (pl.n_vtiles + tps - 1) / tps;
     const int sblocks = (strips + kBlockS - 1) / kBlockS;
     int blocks = pl.n_tblocks * sblocks;
