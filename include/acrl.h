@@ -289,6 +289,7 @@ typedef struct acrl_reduce_desc {
 acrl_status acrl_reduce_workspace_size(int64_t B, int64_t L, int64_t n_groups, size_t* bytes);
 acrl_status acrl_discrepancy_reduce(const acrl_reduce_desc* desc, void* stream);
 
+
 /* ======================================================================== */
 /* a8  acrl_controller_step -- ACRL per-token weights                       */
 /* ======================================================================== *
@@ -310,6 +311,10 @@ acrl_status acrl_discrepancy_reduce(const acrl_reduce_desc* desc, void* stream);
  * Requirements: X > 0, gamma > 0, C > 1 (Sec. 4.1); k > 0 for CONTINUOUS;
  * seq_sum_logratio non-NULL for MIS; the arrays y_level reads non-NULL for
  * ACRL and FALLBACK.
+ * Undefined inputs give NaN, never the clip C: a valid slot whose log-prob is
+ * NaN (acrl_score_pi_mu's mark of an invalid token id) gets weight NaN, and a
+ * response whose group id lies outside [0, n_groups) gets alpha = NaN and
+ * weight = NaN under ACRL_Y_GROUP (ACRL and FALLBACK modes).
  */
 typedef struct acrl_controller_desc {
   int64_t B;

@@ -90,7 +90,7 @@ def lib() -> ctypes.CDLL:
         L.acrl_ref_discrepancy_reduce.restype = I32
         L.acrl_ref_discrepancy_reduce.argtypes = [I64, I64, P, P, P, P, P, P, I64] + [P] * 8
         L.acrl_ref_controller_step.restype = I32
-        L.acrl_ref_controller_step.argtypes = [I64, I64, P, P, P, P, P, I32, I32, P, P, P,
+        L.acrl_ref_controller_step.argtypes = [I64, I64, P, P, I64, P, P, P, I32, I32, P, P, P,
                                                D, D, D, I32, D, P, P]
         L.acrl_ref_philox4x32_10.restype = None
         L.acrl_ref_philox4x32_10.argtypes = [P, P, P]
@@ -279,7 +279,8 @@ def discrepancy_reduce(B: int, L: int, logp_pi, logp_mu, mask, group_of_seq, n_g
 # ---------------------------------------------------------------- a8
 def controller_step(B: int, L: int, mask, group_of_seq, logp_pi, logp_mu, adv,
                     adv_per_token: bool, y_level: int, seq_mean_d, group_y, stats,
-                    X: float, gamma: float, C: float, mode: int = 0, k: float = 1.0):
+                    X: float, gamma: float, C: float, mode: int = 0, k: float = 1.0,
+                    n_groups: Optional[int] = None):
     m = _c(mask, np.uint8).reshape(-1)
     g = _c(group_of_seq, np.int32)
     lp_p, lp_m = _c(logp_pi, np.float64).reshape(-1), _c(logp_mu, np.float64).reshape(-1)
@@ -289,7 +290,8 @@ def controller_step(B: int, L: int, mask, group_of_seq, logp_pi, logp_mu, adv,
     st = None if stats is None else _c(stats, np.float64)
     alpha = np.zeros(B * L)
     weight = np.zeros(B * L)
-    _check(lib().acrl_ref_controller_step(B, L, _p(m), _p(g), _p(lp_p), _p(lp_m), _p(a),
+    ng = len(group_y) if (n_groups is None and group_y is not None) else (n_groups or 0)
+    _check(lib().acrl_ref_controller_step(B, L, _p(m), _p(g), int(ng), _p(lp_p), _p(lp_m), _p(a),
                                           int(bool(adv_per_token)), y_level, _p(smd), _p(gy),
                                           _p(st), X, gamma, C, int(mode), float(k), _p(alpha),
                                           _p(weight)),

@@ -481,7 +481,7 @@ static double sign_of(double a) { return (a > 0) - (a < 0); }
  * multiplies the clipped surrogate's gradient.  pi/mu = exp(logp_pi - logp_mu).
  */
 int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
-                             const int32_t* group_of_seq,
+                             const int32_t* group_of_seq, int64_t n_groups,
                              const double* logp_pi, const double* logp_mu,
                              const double* adv, int adv_per_token, int y_level,
                              const double* seq_mean_d, const double* group_y,
@@ -498,7 +498,8 @@ int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
       Y = seq_mean_d[i];
     } else if (y_level == REF_Y_GROUP) {
       if (!group_y || !group_of_seq) return -1;
-      Y = group_y[group_of_seq[i]];
+      /* a response outside every group has no Y */
+      Y = (group_of_seq[i] >= 0 && group_of_seq[i] < n_groups) ? group_y[group_of_seq[i]] : NAN;
     } else if (y_level == REF_Y_BATCH) {
       if (!stats) return -1;
       Y = stats[REF_STAT_Y_BATCH];
@@ -517,20 +518,22 @@ int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
       if (mask[t]) {
         const double A = adv_per_token ? adv[t] : adv[i];
         const double ratio = exp(logp_pi[t] - logp_mu[t]); /* pi / mu */
+        /* min(x, C) of an undefined x is undefined: NaN stays NaN */
         if (mode == REF_CTRL_TIS) {
           a = 1.0;
-          wt = ratio < C ? ratio : C;
+          wt = isnan(ratio) ? NAN : (ratio < C ? ratio : C);
         } else if (mode == REF_CTRL_MIS) {
           a = 1.0;
-          wt = rho_seq <= C ? rho_seq : 0.0;
+          wt = isnan(rho_seq) ? NAN : (rho_seq <= C ? rho_seq : 0.0);
         } else if (mode == REF_CTRL_FALLBACK && Y < X) {
           a = 0.0;
           wt = 1.0;
         } else {
           if (mode == REF_CTRL_CONTINUOUS) a = -k * sign_of(A);
           else a = gamma * sign_of(A) * (1.0 - Y / X);
-          const double rho = pow(ratio, a);
-          wt = rho < C ? rho : C;
+          /* (pi/mu)^alpha; pow() would give 1 for a NaN ratio at alpha = 0 */
+          const double rho = (isnan(ratio) || isnan(a)) ? NAN : pow(ratio, a);
+          wt = isnan(rho) ? NAN : (rho < C ? rho : C);
         }
       }
       if (alpha) alpha[t] = a;

@@ -140,9 +140,13 @@ int acrl_ref_discrepancy_reduce(int64_t B, int64_t L,
  *               rho_i = product of rho_t over the valid tokens of i
  *   CONTINUOUS: alpha = -k sign(A),              weight = min(rho_t^alpha, C)
  *   FALLBACK:   Y < X: alpha = 0, weight = 1 (plain GRPO); else as ACRL
- * Requires X > 0, gamma > 0, C > 1, k > 0 (k is read in CONTINUOUS only).  */
+ * Requires X > 0, gamma > 0, C > 1, k > 0 (k is read in CONTINUOUS only).
+ * An undefined input gives an undefined weight (NaN), never the clip C: a
+ * NaN log-prob (the scorer's mark of an invalid token id), a NaN ratio, or
+ * a response whose group id lies outside [0, n_groups) (its Y is undefined;
+ * its alpha is NaN as well).                                               */
 int acrl_ref_controller_step(int64_t B, int64_t L, const uint8_t* mask,
-                             const int32_t* group_of_seq,
+                             const int32_t* group_of_seq, int64_t n_groups,
                              const double* logp_pi, const double* logp_mu,
                              const double* adv, int adv_per_token, int y_level,
                              const double* seq_mean_d, const double* group_y,

@@ -189,15 +189,23 @@ def _dev(t: torch.Tensor, dtype, name: str):
     return t
 
 
-_ws_cache: Dict[torch.device, torch.Tensor] = {}
+_ws_cache: Dict[tuple, torch.Tensor] = {}
 
 
-def _workspace(nbytes: int, device) -> torch.Tensor:
-    """A cached device byte buffer of at least nbytes (grown on demand)."""
-    buf = _ws_cache.get(device)
+def _workspace(nbytes: int, device, stream=None) -> torch.Tensor:
+    """A cached device byte buffer of at least nbytes for calls on `stream`
+    (the current stream if None), grown on demand.  One buffer per (device,
+    stream): calls on one stream run in order, so they may share it, and a
+    buffer is allocated on the stream that uses it, so torch's allocator
+    recycles a replaced one only after that stream's earlier work."""
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    key = (torch.device(device), s.cuda_stream)
+    buf = _ws_cache.get(key)
     if buf is None or buf.numel() < nbytes:
-        buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
-        _ws_cache[device] = buf
+        _ws_cache.pop(key, None)
+        with torch.cuda.stream(s):
+            buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        _ws_cache[key] = buf
     return buf
 
 
@@ -229,7 +237,7 @@ def acrl_quantize_fp8(x: torch.Tensor, scaling: int, rounding: int = ROUND_NEARE
     nb = _SZ()
     _check(lib().acrl_quantize_workspace_size(rows, cols, scaling, ctypes.byref(nb)),
            "acrl_quantize_workspace_size")
-    ws = _workspace(nb.value, x.device) if nb.value else None
+    ws = _workspace(nb.value, x.device, stream) if nb.value else None
     _check(lib().acrl_quantize_fp8(_ptr(x), rows, cols, ld, scaling, rounding, _ptr(q), _ptr(scales),
                                    _ptr(ws), nb.value, _stream(stream)), "acrl_quantize_fp8")
     return q, scales
@@ -281,7 +289,7 @@ def acrl_score_pi_mu(h, w, hq, hq_scales, wq, wq_scales, mu_scaling: int, token_
     else:
         _check(lib().acrl_score_workspace_size(n_rows, d, V, mu_scaling, ctypes.byref(nb)),
                "acrl_score_workspace_size")
-    ws = _workspace(nb.value, dev)
+    ws = _workspace(nb.value, dev, stream)
     desc = ScoreDesc(n_rows=n_rows, d=d, V=V, h=_ptr(h), w=_ptr(w), hq=_ptr(hq),
                      hq_scales=_ptr(hq_scales), wq=_ptr(wq), wq_scales=_ptr(wq_scales),
                      mu_scaling=mu_scaling, inv_temperature=float(inv_temperature),
@@ -316,7 +324,7 @@ def acrl_sample_mu(hq, hq_scales, wq, wq_scales, mu_scaling: int, seed: int, row
     nb = _SZ()
     _check(lib().acrl_score_workspace_size(n_rows, d, V, mu_scaling, ctypes.byref(nb)),
            "acrl_score_workspace_size")
-    ws = _workspace(nb.value, dev)
+    ws = _workspace(nb.value, dev, stream)
     desc = SampleDesc(n_rows=n_rows, d=d, V=V, hq=_ptr(hq), hq_scales=_ptr(hq_scales), wq=_ptr(wq),
                       wq_scales=_ptr(wq_scales), mu_scaling=mu_scaling,
                       inv_temperature=float(inv_temperature), seed=int(seed) & (2 ** 64 - 1),
@@ -337,33 +345,47 @@ def acrl_trace_score_events(events) -> None:
 
 
 # ------------------------------------------------------------------ a6/a7
-def acrl_discrepancy_reduce(B: int, L: int, n_groups: int, logp_pi, logp_mu, mask, group_of_seq,
-                            entropy_pi=None, entropy_mu=None, want_d_tok: bool = True,
-                            stream=None) -> dict:
+def _reduce(fn_name: str, B: int, L: int, n_groups: int, logp_pi, logp_mu, mask, group_of_seq,
+            entropy_pi, entropy_mu, want_d_tok: bool, stream, use_workspace: bool, out=None) -> dict:
     dev = logp_pi.device
-    out = dict(
-        d_tok=torch.empty(B * L, dtype=torch.float32, device=dev) if want_d_tok else None,
-        seq_len=torch.empty(B, dtype=torch.int32, device=dev),
-        seq_sum_d=torch.empty(B, dtype=torch.float64, device=dev),
-        seq_sum_logratio=torch.empty(B, dtype=torch.float64, device=dev),
-        seq_mean_d=torch.empty(B, dtype=torch.float32, device=dev),
-        group_y=torch.empty(n_groups, dtype=torch.float32, device=dev),
-        group_nseq=torch.empty(n_groups, dtype=torch.int32, device=dev),
-        stats=torch.empty(N_STATS, dtype=torch.float64, device=dev),
-    )
-    nb = _SZ()
-    _check(lib().acrl_reduce_workspace_size(B, L, n_groups, ctypes.byref(nb)), "acrl_reduce_workspace_size")
-    ws = torch.empty(max(nb.value, 256), dtype=torch.uint8, device=dev)
+    if out is None:
+        out = dict(
+            d_tok=torch.empty(B * L, dtype=torch.float32, device=dev) if want_d_tok else None,
+            seq_len=torch.empty(B, dtype=torch.int32, device=dev),
+            seq_sum_d=torch.empty(B, dtype=torch.float64, device=dev),
+            seq_sum_logratio=torch.empty(B, dtype=torch.float64, device=dev),
+            seq_mean_d=torch.empty(B, dtype=torch.float32, device=dev),
+            group_y=torch.empty(n_groups, dtype=torch.float32, device=dev),
+            group_nseq=torch.empty(n_groups, dtype=torch.int32, device=dev),
+            stats=torch.empty(N_STATS, dtype=torch.float64, device=dev),
+        )
+    ws = None
+    nbytes = 0
+    if use_workspace:
+        nb = _SZ()
+        _check(lib().acrl_reduce_workspace_size(B, L, n_groups, ctypes.byref(nb)), "acrl_reduce_workspace_size")
+        ws = _workspace(nb.value, dev, stream)
+        nbytes = nb.value
     desc = ReduceDesc(B=B, L=L, n_groups=n_groups, logp_pi=_ptr(logp_pi), logp_mu=_ptr(logp_mu),
                       entropy_pi=_ptr(entropy_pi), entropy_mu=_ptr(entropy_mu), mask=_ptr(mask),
                       group_of_seq=_ptr(group_of_seq), d_tok=_ptr(out["d_tok"]),
                       seq_len=_ptr(out["seq_len"]), seq_sum_d=_ptr(out["seq_sum_d"]),
                       seq_sum_logratio=_ptr(out["seq_sum_logratio"]), seq_mean_d=_ptr(out["seq_mean_d"]),
                       group_y=_ptr(out["group_y"]), group_nseq=_ptr(out["group_nseq"]),
-                      stats=_ptr(out["stats"]), workspace=_ptr(ws), workspace_bytes=ws.numel())
-    _check(lib().acrl_discrepancy_reduce(ctypes.byref(desc), _stream(stream)), "acrl_discrepancy_reduce")
-    out["_workspace"] = ws  # keep alive until the stream has consumed it
+                      stats=_ptr(out["stats"]), workspace=_ptr(ws), workspace_bytes=nbytes)
+    _check(getattr(lib(), fn_name)(ctypes.byref(desc), _stream(stream)), fn_name)
     return out
+
+
+def acrl_discrepancy_reduce(B: int, L: int, n_groups: int, logp_pi, logp_mu, mask, group_of_seq,
+                            entropy_pi=None, entropy_mu=None, want_d_tok: bool = True,
+                            stream=None) -> dict:
+    """Per-token d, per-response / per-group / batch reductions (a6/a7).
+    Returns a dict of device tensors (d_tok, seq_len, seq_sum_d,
+    seq_sum_logratio, seq_mean_d, group_y, group_nseq, stats)."""
+    return _reduce("acrl_discrepancy_reduce", B, L, n_groups, logp_pi, logp_mu, mask, group_of_seq,
+                   entropy_pi, entropy_mu, want_d_tok, stream, True)
+
 
 
 # ------------------------------------------------------------------ a8
@@ -407,14 +429,13 @@ def acrl_surrogate(B: int, L: int, n_groups: int, mask, group_of_seq, logp_new, 
     loss = torch.empty(1, dtype=torch.float64, device=dev)
     nb = _SZ()
     _check(lib().acrl_surrogate_workspace_size(B, n_groups, ctypes.byref(nb)), "acrl_surrogate_workspace_size")
-    ws = torch.empty(max(nb.value, 256), dtype=torch.uint8, device=dev)
+    ws = _workspace(nb.value, dev, stream)
     desc = SurrogateDesc(B=B, L=L, n_groups=n_groups, mask=_ptr(mask), group_of_seq=_ptr(group_of_seq),
                          logp_new=_ptr(logp_new), logp_old=_ptr(logp_old), adv=_ptr(adv),
                          adv_per_token=int(bool(adv_per_token)), eps_low=float(eps_low),
                          eps_high=float(eps_high), weight=_ptr(weight), coef=_ptr(coef), loss=_ptr(loss),
-                         workspace=_ptr(ws), workspace_bytes=ws.numel())
+                         workspace=_ptr(ws), workspace_bytes=nb.value)
     _check(lib().acrl_surrogate(ctypes.byref(desc), _stream(stream)), "acrl_surrogate")
-    coef._acrl_ws = ws  # keep the workspace alive until the stream has consumed it
     return coef, loss
 
 
@@ -438,7 +459,7 @@ def acrl_lm_head_backward(h, w, token_ids, coef, lse, inv_temperature: float = 1
     nb = _SZ()
     _check(lib().acrl_backward_workspace_size(n_rows, d, V, int(token_chunk), ctypes.byref(nb)),
            "acrl_backward_workspace_size")
-    ws = _workspace(nb.value, dev)
+    ws = _workspace(nb.value, dev, stream)
     desc = BackwardDesc(n_rows=n_rows, d=d, V=V, h=_ptr(h), w=_ptr(w), token_ids=_ptr(token_ids),
                         row_slot=_ptr(row_slot), coef=_ptr(coef), lse=_ptr(lse),
                         inv_temperature=float(inv_temperature), dh=_ptr(dh if want_dh else None),

@@ -343,6 +343,9 @@ __global__ __launch_bounds__(kBatchThreads) void reduce_batch_kernel(acrl_reduce
 // Eq. ACRL, token-level TIS (Eq. tis_objective), sequence-level MIS (Eq.
 // mis_objective, from the fp64 per-sequence log-ratio sums of the reduce),
 // and the continuous-reduction / fallback-to-GRPO ablations of Sec. 5.
+// min(x, C) of an undefined x is undefined: a NaN log-ratio (an invalid
+// token id) or a NaN Y (a group id outside [0, n_groups)) gives weight NaN,
+// not the clip C.
 __global__ __launch_bounds__(256) void controller_kernel(acrl_controller_desc p) {
   const int64_t n = p.B * p.L;
   const double X = p.X, gamma = p.gamma, lnC = log((double)p.C), C = p.C;
@@ -357,10 +360,10 @@ __global__ __launch_bounds__(256) void controller_kernel(acrl_controller_desc p)
       if (p.mode == ACRL_CTRL_MIS) {
         const double s = p.seq_sum_logratio[i];  // ln rho_i
         a_out = 1.0f;
-        w_out = s <= lnC ? (float)exp(s) : 0.0f;
+        w_out = isnan(s) ? __builtin_nanf("") : (s <= lnC ? (float)exp(s) : 0.0f);
       } else if (p.mode == ACRL_CTRL_TIS) {
         a_out = 1.0f;
-        w_out = (float)(lr < lnC ? exp(lr) : C);
+        w_out = isnan(lr) ? __builtin_nanf("") : (float)(lr < lnC ? exp(lr) : C);
       } else {
         double alpha;
         bool grpo = false;
@@ -381,9 +384,9 @@ __global__ __launch_bounds__(256) void controller_kernel(acrl_controller_desc p)
           a_out = 0.0f;
           w_out = 1.0f;
         } else {
-          const double e = alpha * lr;  // ln rho
+          const double e = alpha * lr;  // ln rho (NaN if alpha or lr is)
           a_out = (float)alpha;
-          w_out = (float)(e < lnC ? exp(e) : C);
+          w_out = isnan(e) ? __builtin_nanf("") : (float)(e < lnC ? exp(e) : C);
         }
       }
     }

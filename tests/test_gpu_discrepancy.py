@@ -216,3 +216,48 @@ def test_reduce_empty_and_all_masked(B, L, ng):
     assert np.array_equal(got["group_nseq"], ref["group_nseq"])
     if B * L:
         assert np.all(got["d_tok"] == 0)
+
+
+@pytest.mark.parametrize("mode", [oracle.CTRL_ACRL, oracle.CTRL_TIS, oracle.CTRL_MIS, oracle.CTRL_CONTINUOUS,
+                                  oracle.CTRL_FALLBACK])
+def test_controller_undefined_inputs_give_nan(mode):
+    # a NaN log-prob in a valid slot (the scorer's mark of an invalid token id)
+    # and responses whose group id lies outside [0, n_groups): weight NaN on
+    # both sides (never the clip C), masked slots 0, the rest as the oracle
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    B, L, ng = 8, 40, 3
+    mask, lp_pi, lp_mu, _, _, g = _batch(B, L, ng, 41)
+    mask[:, 0] = 1
+    lp_pi[2, 0] = np.nan
+    lp_mu[5, 0] = np.nan
+    red = _oracle_y(B, L, ng, mask, np.nan_to_num(lp_pi), np.nan_to_num(lp_mu), g)
+    red["seq_sum_logratio"] = np.where(np.isnan(lp_pi - lp_mu).any(axis=1), np.nan, red["seq_sum_logratio"])
+    g = g.copy()
+    g[6], g[7] = ng, -1
+    adv = np.random.default_rng(42).normal(size=B).astype(np.float32)
+    adv[2] = 0.0  # alpha = 0 must not turn the undefined ratio into 1
+    X = float(red["stats"][0]) * 0.5
+    t = lambda a: up(torch, dev, np.ascontiguousarray(a).reshape(-1))
+    alpha, weight = acrl.acrl_controller_step(
+        B, L, ng, t(mask), up(torch, dev, g), t(lp_pi), t(lp_mu), t(adv), False, oracle.Y_GROUP,
+        t(red["seq_mean_d"]), t(red["group_y"]), t(red["stats"]), X, 0.65, 3.0, mode=mode, k=1.0,
+        seq_sum_logratio=up(torch, dev, red["seq_sum_logratio"]))
+    torch.cuda.synchronize()
+    a_ref, w_ref = oracle.controller_step(B, L, mask, g, lp_pi, lp_mu, adv, False, oracle.Y_GROUP,
+                                          red["seq_mean_d"], red["group_y"], red["stats"],
+                                          float(np.float32(X)), float(np.float32(0.65)), 3.0, mode=mode,
+                                          k=1.0, n_groups=ng)
+    wg, ag = down(weight).reshape(B, L), down(alpha).reshape(B, L)
+    assert np.array_equal(np.isnan(wg), np.isnan(w_ref.reshape(B, L)))
+    assert np.array_equal(np.isnan(ag), np.isnan(a_ref.reshape(B, L)))
+    assert np.isnan(wg[2, 0]) and np.isnan(wg[5, 0])
+    if mode in (oracle.CTRL_ACRL, oracle.CTRL_FALLBACK):
+        on = mask[6:].astype(bool)
+        assert np.isnan(wg[6:][on]).all() and np.isnan(ag[6:][on]).all()
+    assert np.all(wg[mask == 0] == 0)
+    rtol = 1e-9 * L if mode == oracle.CTRL_MIS else 2 ** -23
+    np.testing.assert_allclose(wg, w_ref.reshape(B, L).astype(np.float32), rtol=max(rtol, 2 ** -23), atol=1e-30,
+                               equal_nan=True)
+    np.testing.assert_allclose(ag, a_ref.reshape(B, L).astype(np.float32), rtol=2 ** -23, atol=1e-30,
+                               equal_nan=True)

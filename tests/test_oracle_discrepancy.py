@@ -321,3 +321,53 @@ def test_controller_rejects_bad_mode_or_k():
         _ctrl_mode(0.2, 0.4, 1.0, 0.02, 7)
     with pytest.raises(ValueError):
         _ctrl_mode(0.2, 0.4, 1.0, 0.02, oracle.CTRL_CONTINUOUS, k=0.0)
+
+
+# ------------------------------------------------------------ undefined inputs
+# min(rho, C) is defined for a ratio rho; an undefined ratio (a NaN log-prob,
+# the scorer's mark of an invalid token id) or an undefined Y (a response
+# outside every group) leaves the weight undefined: NaN, never the clip C.
+@pytest.mark.parametrize("mode", [oracle.CTRL_ACRL, oracle.CTRL_TIS, oracle.CTRL_CONTINUOUS,
+                                  oracle.CTRL_FALLBACK])
+@pytest.mark.parametrize("A", [1.0, -1.0, 0.0])
+def test_nan_logprob_gives_nan_weight(mode, A):
+    # Y = 0.026 > X: FALLBACK takes the ACRL branch; A = 0 (alpha = 0) must
+    # not turn the undefined ratio into 1
+    a, w = _ctrl_mode(float("nan"), 0.4, A, 0.026, mode)
+    assert math.isnan(w)
+    a, w = _ctrl_mode(0.2, float("nan"), A, 0.026, mode)
+    assert math.isnan(w)
+
+
+def test_nan_logprob_mis_weights_its_sequence_nan():
+    B, L = 2, 3
+    mask = np.ones((B, L), np.uint8)
+    lp_mu = np.log(np.full((B, L), 0.3))
+    lp_pi = lp_mu.copy()
+    lp_pi[0, 1] = float("nan")
+    _, w = oracle.controller_step(B, L, mask, np.zeros(B, np.int32), lp_pi, lp_mu, np.ones(B), False,
+                                  oracle.Y_BATCH, None, None, np.zeros(oracle.N_STATS), 0.013, 0.65, 3.0,
+                                  mode=oracle.CTRL_MIS)
+    w = w.reshape(B, L)
+    assert np.isnan(w[0]).all() and np.all(w[1] == 1.0)
+
+
+@pytest.mark.parametrize("mode", [oracle.CTRL_ACRL, oracle.CTRL_FALLBACK])
+def test_group_outside_range_gives_nan(mode):
+    B, L, ng = 3, 2, 2
+    mask = np.ones((B, L), np.uint8)
+    lp_pi = np.log(np.full((B, L), 0.2))
+    lp_mu = np.log(np.full((B, L), 0.4))
+    g = np.array([0, 2, -1], np.int32)  # responses 1 and 2 belong to no group
+    gy = np.array([0.026, 0.026])
+    alpha, w = oracle.controller_step(B, L, mask, g, lp_pi, lp_mu, np.ones(B), False, oracle.Y_GROUP, None,
+                                      gy, None, 0.013, 0.65, 3.0, mode=mode, n_groups=ng)
+    alpha, w = alpha.reshape(B, L), w.reshape(B, L)
+    assert np.isnan(alpha[1:]).all() and np.isnan(w[1:]).all()
+    # response 0: alpha = 0.65 (1 - 2) = -0.65, rho = (0.2/0.4)^-0.65 (the worked value)
+    assert np.allclose(alpha[0], -0.65) and np.allclose(w[0], 1.569168, atol=1e-6)
+    # masked slots stay 0 whatever the group
+    mask[1, 1] = 0
+    alpha, w = oracle.controller_step(B, L, mask, g, lp_pi, lp_mu, np.ones(B), False, oracle.Y_GROUP, None,
+                                      gy, None, 0.013, 0.65, 3.0, mode=mode, n_groups=ng)
+    assert alpha.reshape(B, L)[1, 1] == 0 and w.reshape(B, L)[1, 1] == 0
