@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ACRL_ABI_VERSION 4
+#define ACRL_ABI_VERSION 5
 
 typedef int acrl_status;
 enum {
@@ -289,6 +289,25 @@ typedef struct acrl_reduce_desc {
 acrl_status acrl_reduce_workspace_size(int64_t B, int64_t L, int64_t n_groups, size_t* bytes);
 acrl_status acrl_discrepancy_reduce(const acrl_reduce_desc* desc, void* stream);
 
+/* acrl_discrepancy_reduce_noalloc -- the same reduce for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  It computes exactly what
+ * acrl_discrepancy_reduce computes, with the same kernels, but takes its
+ * intermediate records from a fixed device array of ACRL_REDUCE_SCRATCH_BYTES
+ * that the library holds on each device it runs on, for the life of the
+ * process; desc->workspace and desc->workspace_bytes are ignored.  It calls
+ * no hipMalloc / hipFree and allocates nothing.
+ * Limit: acrl_reduce_workspace_size(B, L, n_groups) (64 bytes per response,
+ * 144 per group, plus alignment) must not exceed ACRL_REDUCE_SCRATCH_BYTES
+ * (4 MiB: e.g. 49152 responses in 4096 groups); larger batches get
+ * ACRL_ERR_WORKSPACE.
+ * Every call on a device shares that device's array, which keeps the last
+ * call's contents (each call clears what it needs): calls that overlap in
+ * time on one device (different streams or threads) race and must be
+ * serialized by the caller.  Other requirements and errors as
+ * acrl_discrepancy_reduce.                                                  */
+#define ACRL_REDUCE_SCRATCH_BYTES (4u << 20)
+acrl_status acrl_discrepancy_reduce_noalloc(const acrl_reduce_desc* desc, void* stream);
 
 /* ======================================================================== */
 /* a8  acrl_controller_step -- ACRL per-token weights                       */

@@ -30,7 +30,7 @@ EXPORTED = [
     "acrl_status_string", "acrl_last_error", "acrl_abi_version", "acrl_abi_struct_sizes",
     "acrl_quantize_workspace_size", "acrl_quantize_fp8", "acrl_fp8_encode",
     "acrl_score_workspace_size", "acrl_score_div_workspace_size", "acrl_score_pi_mu", "acrl_trace_score_events",
-    "acrl_reduce_workspace_size", "acrl_discrepancy_reduce",
+    "acrl_reduce_workspace_size", "acrl_discrepancy_reduce", "acrl_discrepancy_reduce_noalloc",
     "acrl_controller_step", "acrl_reference_from_groups", "acrl_sample_mu",
     "acrl_surrogate_workspace_size", "acrl_surrogate",
     "acrl_backward_workspace_size", "acrl_lm_head_backward",
@@ -140,6 +140,8 @@ def lib() -> ctypes.CDLL:
         L.acrl_reduce_workspace_size.argtypes = [_I64, _I64, _I64, ctypes.POINTER(_SZ)]
         L.acrl_discrepancy_reduce.restype = _I32
         L.acrl_discrepancy_reduce.argtypes = [ctypes.POINTER(ReduceDesc), _P]
+        L.acrl_discrepancy_reduce_noalloc.restype = _I32
+        L.acrl_discrepancy_reduce_noalloc.argtypes = [ctypes.POINTER(ReduceDesc), _P]
         L.acrl_controller_step.restype = _I32
         L.acrl_controller_step.argtypes = [ctypes.POINTER(ControllerDesc), _P]
         L.acrl_reference_from_groups.restype = _I32
@@ -386,6 +388,15 @@ def acrl_discrepancy_reduce(B: int, L: int, n_groups: int, logp_pi, logp_mu, mas
     return _reduce("acrl_discrepancy_reduce", B, L, n_groups, logp_pi, logp_mu, mask, group_of_seq,
                    entropy_pi, entropy_mu, want_d_tok, stream, True)
 
+
+def acrl_discrepancy_reduce_noalloc(B: int, L: int, n_groups: int, logp_pi, logp_mu, mask, group_of_seq,
+                                    entropy_pi=None, entropy_mu=None, want_d_tok: bool = True,
+                                    stream=None, out: Optional[dict] = None) -> dict:
+    """The same reduce on the library's fixed per-device scratch (no
+    workspace).  With `out` (a dict of preallocated output tensors as
+    acrl_discrepancy_reduce returns) nothing is allocated on this path."""
+    return _reduce("acrl_discrepancy_reduce_noalloc", B, L, n_groups, logp_pi, logp_mu, mask, group_of_seq,
+                   entropy_pi, entropy_mu, want_d_tok, stream, False, out)
 
 
 # ------------------------------------------------------------------ a8

@@ -66,6 +66,11 @@ hipError_t launch_surrogate(const acrl_surrogate_desc& desc, hipStream_t s);
 
 size_t reduce_workspace_bytes(int64_t B, int64_t L, int64_t n_groups);
 hipError_t launch_reduce(const acrl_reduce_desc& desc, hipStream_t s);
+// Fixed device scratch of the allocation-free reduce (one copy per device):
+// its device address on the current device, looked up once per device.
+constexpr size_t kReduceScratchBytes = (size_t)ACRL_REDUCE_SCRATCH_BYTES;
+constexpr int kMaxScratchDevices = 64;
+hipError_t reduce_scratch(void** ptr);
 hipError_t launch_controller(const acrl_controller_desc& desc, hipStream_t s);
 
 // ------------------------------------------------------------------ device

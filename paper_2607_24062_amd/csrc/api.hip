@@ -307,6 +307,27 @@ acrl_status acrl_discrepancy_reduce(const acrl_reduce_desc* desc, void* stream) 
   return acrl::hip_status(acrl::launch_reduce(*desc, (hipStream_t)stream), "acrl_discrepancy_reduce launch");
 }
 
+acrl_status acrl_discrepancy_reduce_noalloc(const acrl_reduce_desc* desc, void* stream) {
+  acrl_status st = acrl::validate_reduce(desc);
+  if (st != ACRL_OK) return st;
+  const size_t need = acrl::reduce_workspace_bytes(desc->B, desc->L, desc->n_groups);
+  if (need > acrl::kReduceScratchBytes) {
+    set_error("acrl_discrepancy_reduce_noalloc: B = %lld, n_groups = %lld need %zu scratch bytes, above the "
+              "fixed %zu (use acrl_discrepancy_reduce with a workspace)",
+              (long long)desc->B, (long long)desc->n_groups, need, acrl::kReduceScratchBytes);
+    return ACRL_ERR_WORKSPACE;
+  }
+  st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  void* scratch = nullptr;
+  st = acrl::hip_status(acrl::reduce_scratch(&scratch), "acrl_discrepancy_reduce_noalloc scratch lookup");
+  if (st != ACRL_OK) return st;
+  acrl_reduce_desc d = *desc;
+  d.workspace = scratch;
+  d.workspace_bytes = acrl::kReduceScratchBytes;
+  return acrl::hip_status(acrl::launch_reduce(d, (hipStream_t)stream), "acrl_discrepancy_reduce_noalloc launch");
+}
+
 acrl_status acrl_controller_step(const acrl_controller_desc* d, void* stream) {
   ACRL_REQUIRE(d, "desc is NULL");
   ACRL_REQUIRE(d->B >= 0 && d->L >= 0 && d->n_groups >= 0, "B, L and n_groups must be >= 0");

@@ -15,6 +15,8 @@
 // loads; all sums are fp64 and combined by fixed-shape tree reductions, so
 // results are deterministic (no floating-point atomics).  These kernels are
 // HBM / latency bound; the controller is a plain grid-stride stream.
+#include <mutex>
+
 #include "acrl_internal.h"
 
 namespace acrl {
@@ -569,6 +571,36 @@ hipError_t launch_reduce(const acrl_reduce_desc& p, hipStream_t s) {
   hipLaunchKernelGGL(reduce_batch_kernel, dim3(1), dim3(kBatchThreads), 0, s, p, (const GroupRec*)grec,
                      (const double*)gy, (const double*)gc);
   return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ fixed scratch
+// Device memory for acrl_discrepancy_reduce_noalloc: the reduce's per-response
+// and per-group records live here instead of in a caller workspace.  Each
+// device holds its own copy for the life of the process; host code reaches
+// it only through the address hipGetSymbolAddress returns for that device
+// (the array's name is a host-side stand-in, not a device address).
+static __device__ __align__(256) uint8_t scratch[kReduceScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxScratchDevices];  // device address of `scratch` per device, once looked up
+}  // namespace
+
+hipError_t reduce_scratch(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxScratchDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* a = nullptr;
+    e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!a) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = a;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 hipError_t launch_controller(const acrl_controller_desc& p, hipStream_t s) {
