@@ -4,7 +4,9 @@ One step = the whole hot path over one batch already resident in HBM:
 quantize H for mu (per-tensor FP8), score every valid token under pi (BF16)
 and mu (FP8) with the fused log-softmax, merge, reduce the discrepancy per
 sequence / group / batch, and apply the ACRL controller.  W's quantization
-happens once per weight version and is reported separately.
+and its packed tile image happen once per weight version and are reported
+separately.  After the headline workload (q8b), the other full-size
+workloads (q17b, long, mx) run the same step and land under "workloads".
 
 Usage: python bench.py [--gpus 1] [--steps 5] [--warmup 2] [--workload q8b]
 Prints progress on stderr and ONE JSON line on stdout.
@@ -35,6 +37,130 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def setup(torch, acrl, w, dev):
+    """The workload resident in HBM: inputs, W's quantization and packed
+    image (once per weight version, timed apart) and the rollout's ids drawn
+    from mu (untimed)."""
+    T = inputs.n_valid(w)
+    d, V = w.d, w.V
+    t0 = time.time()
+    H = inputs.hidden_bf16_torch(w, T, dev)
+    W = inputs.weights_bf16_torch(w, dev)
+    slots = torch.from_numpy(inputs.valid_slots(w)).to(dev)
+    mask = torch.from_numpy(inputs.mask(w).reshape(-1)).to(dev)
+    groups = torch.from_numpy(inputs.group_of_seq(w)).to(dev)
+    adv = torch.from_numpy(inputs.advantages(w)).to(dev)
+    torch.cuda.synchronize()
+    log("[%s] inputs generated in %.1fs" % (w.name, time.time() - t0))
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    a, b, c = ev(), ev(), ev()
+    wq, ws = acrl.acrl_quantize_fp8(W, w.scaling)
+    packed = acrl.acrl_pack_weights(W, wq, ws, w.scaling)
+    torch.cuda.synchronize()
+    a.record()
+    acrl.acrl_quantize_fp8(W, w.scaling, q=wq, scales=ws)
+    b.record()
+    acrl.acrl_pack_weights(W, wq, ws, w.scaling, packed=packed)
+    c.record()
+    torch.cuda.synchronize()
+    wq_ms, pw_ms = a.elapsed_time(b), b.elapsed_time(c)
+    wq_bytes = V * d * (2 + 1) + (V * d * 2 if w.scaling == inputs.PER_TENSOR else 0)
+    log("[%s] quantize W: %.3f ms (%.0f GB/s); pack W, Wq: %.3f ms" % (w.name, wq_ms, wq_bytes / wq_ms / 1e6, pw_ms))
+    hq0, hs0 = acrl.acrl_quantize_fp8(H, w.scaling)
+    a.record()
+    ids, _ = acrl.acrl_sample_mu(hq0, hs0, wq, ws, w.scaling, seed=w.seed, inv_temperature=w.inv_temperature,
+                                 want_logp=False, packed_weights=packed)
+    b.record()
+    torch.cuda.synchronize()
+    sample_ms = a.elapsed_time(b)
+    del hq0, hs0
+    log("[%s] ids sampled from mu in %.1f ms" % (w.name, sample_ms))
+    hq = torch.empty((T, d), dtype=torch.uint8, device=dev)
+    if w.scaling == inputs.PER_TENSOR:
+        hs = torch.empty(1, dtype=torch.float32, device=dev)
+    elif w.scaling == inputs.PER_ROW:
+        hs = torch.empty(T, dtype=torch.float32, device=dev)
+    else:
+        hs = torch.empty((T, d // 32), dtype=torch.uint8, device=dev)
+    outs = {k: torch.zeros(w.slots, dtype=torch.float32, device=dev)
+            for k in ("logp_pi", "logp_mu", "entropy_pi", "entropy_mu")}
+    return dict(w=w, T=T, H=H, W=W, wq=wq, ws=ws, packed=packed, slots=slots, mask=mask, groups=groups, adv=adv,
+                ids=ids, hq=hq, hs=hs, outs=outs, X=None, wq_ms=wq_ms, wq_bytes=wq_bytes, pw_ms=pw_ms,
+                sample_ms=sample_ms)
+
+
+def step(acrl, S, ev=None):
+    """One pass of the hot path.  With ev (a list of 6 events) the pass is
+    split at the call boundaries: quantize H | pi scoring | mu scoring |
+    reduce | controller, pi and mu scored by separate calls (the same
+    kernels the fused call launches) so that each can be timed alone."""
+    w = S["w"]
+    rec = (lambda k: ev[k].record()) if ev is not None else (lambda k: None)
+    rec(0)
+    acrl.acrl_quantize_fp8(S["H"], w.scaling, q=S["hq"], scales=S["hs"])
+    rec(1)
+    kw = dict(inv_temperature=w.inv_temperature, out_slot=S["slots"], n_slots=w.slots, outputs=S["outs"],
+              want=("entropy",), packed_weights=S["packed"])
+    args = (S["H"], S["W"], S["hq"], S["hs"], S["wq"], S["ws"], w.scaling, S["ids"])
+    if ev is None:
+        sc = acrl.acrl_score_pi_mu(*args, **kw)
+    else:
+        sc = acrl.acrl_score_pi_mu(*args, policies=acrl.POLICY_PI, **kw)
+        rec(2)
+        sc = acrl.acrl_score_pi_mu(*args, policies=acrl.POLICY_MU, **kw)
+    rec(3)
+    red = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, sc["logp_pi"], sc["logp_mu"], S["mask"], S["groups"],
+                                       entropy_pi=sc["entropy_pi"], entropy_mu=sc["entropy_mu"], want_d_tok=False)
+    rec(4)
+    # X: the step-0 batch discrepancy (read once, outside the timed steps)
+    X = S["X"] if S["X"] is not None else 1.0
+    acrl.acrl_controller_step(w.B, w.L, w.n_prompts, S["mask"], S["groups"], sc["logp_pi"], sc["logp_mu"], S["adv"],
+                              False, acrl.Y_GROUP, red["seq_mean_d"], red["group_y"], red["stats"], X, 0.65, 3.0,
+                              want_alpha=False)
+    rec(5)
+    return red
+
+
+def measure(torch, acrl, S, steps, warmup):
+    """Warm-up (step 0 calibrates X, Sec. 4.1), the timed steps of the whole
+    path, then one split pass per step for the per-kernel times."""
+    w, T = S["w"], S["T"]
+    d, V = w.d, w.V
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    t0 = time.time()
+    red = step(acrl, S)
+    torch.cuda.synchronize()
+    S["X"] = max(float(red["stats"][0].item()), 1e-12)
+    for _ in range(max(warmup - 1, 0)):
+        step(acrl, S)
+    torch.cuda.synchronize()
+    log("[%s] warmup %d steps in %.1fs; X = %.4g" % (w.name, warmup, time.time() - t0, S["X"]))
+    start, end = ev(), ev()
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        step(acrl, S)
+    end.record()
+    torch.cuda.synchronize()
+    ms_per_step = start.elapsed_time(end) / steps
+    evs = [[ev() for _ in range(6)] for _ in range(steps)]
+    for k in range(steps):
+        red = step(acrl, S, evs[k])
+    torch.cuda.synchronize()
+    seg = lambda i, j: float(np.mean([evs[k][i].elapsed_time(evs[k][j]) for k in range(steps)]))
+    t = {"quantize_h": seg(0, 1), "score_pi_call": seg(1, 2), "score_mu_call": seg(2, 3), "reduce": seg(3, 4),
+         "controller": seg(4, 5)}
+    stats = red["stats"].cpu().numpy()
+    log("[%s] per step %.3f ms | " % (w.name, ms_per_step) + " | ".join("%s %.3f" % kv for kv in t.items()))
+    log("[%s] batch stats:" % w.name, dict(zip(acrl.STAT_NAMES, [float(x) for x in stats])))
+    flops = 2.0 * T * V * d           # per precision, algorithmic
+    ideal_ms = (flops / (PEAK_TFLOPS["bf16"] * 1e12) + flops / (PEAK_TFLOPS["fp8"] * 1e12)) * 1e3
+    return dict(ms_per_step=ms_per_step, kernel_ms=t, flops=flops, ideal_ms=ideal_ms,
+                pi_frac=flops / (t["score_pi_call"] * 1e-3) / 1e12 / PEAK_TFLOPS["bf16"],
+                mu_frac=flops / (t["score_mu_call"] * 1e-3) / 1e12 / PEAK_TFLOPS["fp8"],
+                mfma_frac_combined=ideal_ms / ms_per_step, stats=stats)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -49,6 +175,8 @@ def main():
                     help="skip the surrogate + LM-head backward leg")
     ap.add_argument("--no-library", action="store_true",
                     help="skip the vendor-library GEMM leg (hipBLASLt through torch, no softmax)")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the other full-size workloads (q17b, long, mx after the headline)")
     ap.add_argument("--counters", action="store_true",
                     help="copy calibration + one step only (for rocprofv3 --pmc passes)")
     args = ap.parse_args()
@@ -64,87 +192,10 @@ def main():
     torch.cuda.set_device(dev)
     acrl.lib()
     w = inputs.WORKLOADS[args.workload]
-    T = inputs.n_valid(w)
-    d, V = w.d, w.V
-    log("workload:", w.describe(), "| valid tokens", T, "of", w.slots, "slots")
-
-    # ---------------- inputs resident in HBM
-    t0 = time.time()
-    H = inputs.hidden_bf16_torch(w, T, dev)
-    W = inputs.weights_bf16_torch(w, dev)
-    slots = torch.from_numpy(inputs.valid_slots(w)).to(dev)
-    mask = torch.from_numpy(inputs.mask(w).reshape(-1)).to(dev)
-    groups = torch.from_numpy(inputs.group_of_seq(w)).to(dev)
-    adv = torch.from_numpy(inputs.advantages(w)).to(dev)
-    torch.cuda.synchronize()
-    log("inputs generated in %.1fs" % (time.time() - t0))
-
-    # ---------------- W quantization (once per weight version)
-    ev = lambda: torch.cuda.Event(enable_timing=True)
-    a, b = ev(), ev()
-    a.record()
-    wq, ws = acrl.acrl_quantize_fp8(W, w.scaling)
-    b.record()
-    torch.cuda.synchronize()
-    a.record()
-    wq, ws = acrl.acrl_quantize_fp8(W, w.scaling, q=wq, scales=ws)
-    b.record()
-    torch.cuda.synchronize()
-    wq_ms = a.elapsed_time(b)
-    wq_bytes = V * d * (2 + 1) + (V * d * 2 if w.scaling == inputs.PER_TENSOR else 0)
-    log("quantize W: %.3f ms (%.0f GB/s)" % (wq_ms, wq_bytes / wq_ms / 1e6))
-
-    # ---------------- the rollout's tokens: drawn from mu (Gumbel-max in the mu kernel), untimed
-    hq0, hs0 = acrl.acrl_quantize_fp8(H, w.scaling)
-    a.record()
-    ids, _ = acrl.acrl_sample_mu(hq0, hs0, wq, ws, w.scaling, seed=w.seed,
-                                 inv_temperature=w.inv_temperature, want_logp=False)
-    b.record()
-    torch.cuda.synchronize()
-    sample_ms = a.elapsed_time(b)
-    del hq0, hs0
-    log("ids sampled from mu in %.1f ms" % sample_ms)
-
-    # ---------------- preallocated step buffers
-    hq = torch.empty((T, d), dtype=torch.uint8, device=dev)
-    if w.scaling == inputs.PER_TENSOR:
-        hs = torch.empty(1, dtype=torch.float32, device=dev)
-    elif w.scaling == inputs.PER_ROW:
-        hs = torch.empty(T, dtype=torch.float32, device=dev)
-    else:
-        hs = torch.empty((T, d // 32), dtype=torch.uint8, device=dev)
-    outs = {k: torch.zeros(w.slots, dtype=torch.float32, device=dev)
-            for k in ("logp_pi", "logp_mu", "entropy_pi", "entropy_mu")}
-    X_ref = [None]
-
-    def step(trace_events=None, qev=None, rev=None):
-        if qev is not None:
-            qev[0].record()
-        acrl.acrl_quantize_fp8(H, w.scaling, q=hq, scales=hs)
-        if qev is not None:
-            qev[1].record()
-        if trace_events is not None:
-            acrl.acrl_trace_score_events(trace_events)
-        sc = acrl.acrl_score_pi_mu(H, W, hq, hs, wq, ws, w.scaling, ids,
-                                   inv_temperature=w.inv_temperature, out_slot=slots,
-                                   n_slots=w.slots, outputs=outs, want=("entropy",))
-        if trace_events is not None:
-            acrl.acrl_trace_score_events(None)
-        if rev is not None:
-            rev[0].record()
-        red = acrl.acrl_discrepancy_reduce(w.B, w.L, w.n_prompts, sc["logp_pi"], sc["logp_mu"], mask,
-                                           groups, entropy_pi=sc["entropy_pi"],
-                                           entropy_mu=sc["entropy_mu"], want_d_tok=False)
-        if rev is not None:
-            rev[1].record()
-        # X: the step-0 batch discrepancy (read once, outside the timed steps)
-        X = X_ref[0] if X_ref[0] is not None else 1.0
-        acrl.acrl_controller_step(w.B, w.L, w.n_prompts, mask, groups, sc["logp_pi"], sc["logp_mu"],
-                                  adv, False, acrl.Y_GROUP, red["seq_mean_d"], red["group_y"],
-                                  red["stats"], X, 0.65, 3.0, want_alpha=False)
-        if rev is not None:
-            rev[2].record()
-        return red
+    log("workload:", w.describe(), "| valid tokens", inputs.n_valid(w), "of", w.slots, "slots")
+    S = setup(torch, acrl, w, dev)
+    T, d, V = S["T"], w.d, w.V
+    H, W, hq, hs, wq, ws, ids, slots = S["H"], S["W"], S["hq"], S["hs"], S["wq"], S["ws"], S["ids"], S["slots"]
 
     if args.counters:
         # a plain copy of COPY_BYTES (read and written once), then one step
@@ -153,64 +204,27 @@ def main():
         torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
-        step()
+        step(acrl, S)
         if not args.no_divergence:
-            divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, 0.0, reps=0)
+            divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["packed"], 0.0, reps=0)
         if not args.no_backward:
-            backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv, 1.0, reps=0)
+            backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["mask"], S["groups"], S["adv"], 1.0,
+                         reps=0)
         if not args.no_library:
             library_leg(torch, w, T, H, W, hq, hs, wq, ws, 1.0, 1.0, reps=0)
         torch.cuda.synchronize()
         log("counters run done")
         return
 
-    # ---------------- warmup (step 0 calibrates X, Sec. 4.1)
-    t0 = time.time()
-    red = step()
-    torch.cuda.synchronize()
-    X_ref[0] = max(float(red["stats"][0].item()), 1e-12)
-    for _ in range(max(args.warmup - 1, 0)):
-        step()
-    torch.cuda.synchronize()
-    log("warmup %d steps in %.1fs; X = %.4g" % (args.warmup, time.time() - t0, X_ref[0]))
-
-    # ---------------- timed steps (whole path), then per-kernel event timing
-    start, end = ev(), ev()
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
-        step()
-    end.record()
-    torch.cuda.synchronize()
-    ms_per_step = start.elapsed_time(end) / args.steps
-
-    K = args.steps
-    tev = [[ev() for _ in range(4)] for _ in range(K)]
-    qev = [[ev(), ev()] for _ in range(K)]
-    rev = [[ev(), ev(), ev()] for _ in range(K)]
-    for e in [x for s in tev for x in s]:
-        e.record()  # materialise the event handles
-    torch.cuda.synchronize()
-    for k in range(K):
-        red = step(tev[k], qev[k], rev[k])
-    torch.cuda.synchronize()
-    t_pi = np.mean([tev[k][0].elapsed_time(tev[k][1]) for k in range(K)])
-    t_mu = np.mean([tev[k][1].elapsed_time(tev[k][2]) for k in range(K)])
-    t_merge = np.mean([tev[k][2].elapsed_time(tev[k][3]) for k in range(K)])
-    t_qh = np.mean([qev[k][0].elapsed_time(qev[k][1]) for k in range(K)])
-    # the score call = operand packing + pi + mu + merge (events: end of quantize -> start of reduce)
-    t_call = np.mean([qev[k][1].elapsed_time(rev[k][0]) for k in range(K)])
-    t_pack = max(t_call - t_pi - t_mu - t_merge, 0.0)
-    t_red = np.mean([rev[k][0].elapsed_time(rev[k][1]) for k in range(K)])
-    t_ctl = np.mean([rev[k][1].elapsed_time(rev[k][2]) for k in range(K)])
-    stats = red["stats"].cpu().numpy()
-    log("per step %.3f ms | quantize H %.3f | pack %.3f | pi %.3f | mu %.3f | merge %.3f | reduce %.3f | "
-        "controller %.3f ms" % (ms_per_step, t_qh, t_pack, t_pi, t_mu, t_merge, t_red, t_ctl))
-    log("batch stats:", dict(zip(acrl.STAT_NAMES, [float(x) for x in stats])))
-
-    flops = 2.0 * T * V * d           # per precision, algorithmic
+    R = measure(torch, acrl, S, args.steps, args.warmup)
+    ms_per_step, t = R["ms_per_step"], R["kernel_ms"]
+    t_pi, t_mu = t["score_pi_call"], t["score_mu_call"]
+    flops = R["flops"]
     ach_pi = flops / (t_pi * 1e-3) / 1e12
     ach_mu = flops / (t_mu * 1e-3) / 1e12
+    # achieved = 2 T V d FLOP per launch / the launch's duration, the duration
+    # being the bench's own events around a call that launches the kernel and
+    # the policy's strip merge (tens of microseconds)
     roof_pi = {"kernel": "score_kernel<bf16> (pi LM head + fused log-softmax)", "bound": "mfma",
                "achieved": round(ach_pi, 1), "peak": PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
                "frac": round(ach_pi / PEAK_TFLOPS["bf16"], 4), "traffic": None,
@@ -236,8 +250,6 @@ def main():
         if row is not None:
             roof["traffic"] = round(row["traffic_bytes"])
             roof["traffic_unit"] = "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
-    # fraction of the combined MFMA roofline: ideal time at both peaks / measured step time
-    ideal_ms = (flops / (PEAK_TFLOPS["bf16"] * 1e12) + flops / (PEAK_TFLOPS["fp8"] * 1e12)) * 1e3
     q_bytes = T * d * 3 + (T * d * 2 if w.scaling == inputs.PER_TENSOR else 0)
 
     value = T / (ms_per_step * 1e-3)
@@ -256,35 +268,56 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.describe(), "valid_tokens": T, "slots": w.slots,
                    "ids": "drawn from mu at tau (Gumbel-max with Philox4x32-10, seed %d), untimed" % w.seed,
-                   "sample_mu_ms": round(sample_ms, 3),
-                   "mfma_frac_combined": round(ideal_ms / ms_per_step, 4),
-                   "kernel_ms": {"quantize_h": round(float(t_qh), 4), "pack": round(float(t_pack), 4),
-                                 "score_pi": round(float(t_pi), 4),
-                                 "score_mu": round(float(t_mu), 4), "merge": round(float(t_merge), 4),
-                                 "reduce": round(float(t_red), 4), "controller": round(float(t_ctl), 4)},
-                   "quantize_h_GBps": round(q_bytes / (t_qh * 1e-3) / 1e9, 1),
-                   "quantize_w_ms": round(wq_ms, 4),
-                   "quantize_w_GBps": round(wq_bytes / (wq_ms * 1e-3) / 1e9, 1),
-                   # one step with the once-per-weight-version quantization of W added in
-                   "all_in_tokens_per_s": round(T / ((ms_per_step + wq_ms) * 1e-3), 1),
-                   "X": X_ref[0]},
+                   "sample_mu_ms": round(S["sample_ms"], 3),
+                   "mfma_frac_combined": round(R["mfma_frac_combined"], 4),
+                   "kernel_ms": {k: round(v, 4) for k, v in t.items()},
+                   "quantize_h_GBps": round(q_bytes / (t["quantize_h"] * 1e-3) / 1e9, 1),
+                   "quantize_w_ms": round(S["wq_ms"], 4),
+                   "quantize_w_GBps": round(S["wq_bytes"] / (S["wq_ms"] * 1e-3) / 1e9, 1),
+                   "pack_w_ms": round(S["pw_ms"], 4),
+                   # one step with the once-per-weight-version quantization and packing of W added in
+                   "all_in_tokens_per_s": round(T / ((ms_per_step + S["wq_ms"] + S["pw_ms"]) * 1e-3), 1),
+                   "X": S["X"]},
         "roofline": dominant,
         "roofline_other": roof_mu if dominant is roof_pi else roof_pi,
     }
 
     line["config"]["hbm_kernels"] = hbm_kernels(torch, acrl, dev, H, w)
+    score_ms = t_pi + t_mu
     if not args.no_divergence:
-        line["divergence"] = divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, t_call)
+        line["divergence"] = divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["packed"],
+                                            score_ms)
     if not args.no_backward:
-        line["backward"] = backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, mask, groups, adv,
-                                        X_ref[0])
-
+        line["backward"] = backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["mask"], S["groups"],
+                                        S["adv"], S["X"])
     if not args.no_library:
         line["library_gemm"] = library_leg(torch, w, T, H, W, hq, hs, wq, ws, t_pi, t_mu)
 
     # ---------------- CPU baseline: the oracle on host cores, bounded sample
     if args.cpu_seconds > 0:
         line["cpu_baseline"] = cpu_baseline(w, T, H, W, args.cpu_seconds)
+    del S, H, W, hq, hs, wq, ws, ids, slots
+    torch.cuda.empty_cache()
+
+    # ---------------- the other full-size workloads: the same step, fewer steps
+    if not args.no_workloads:
+        line["workloads"] = {}
+        for name in ("q17b", "long", "mx"):
+            if name == w.name:
+                continue
+            wl = inputs.WORKLOADS[name]
+            S2 = setup(torch, acrl, wl, dev)
+            R2 = measure(torch, acrl, S2, 2, 1)
+            line["workloads"][name] = {
+                "workload": wl.describe(), "valid_tokens": S2["T"], "steps": 2, "warmup": 1,
+                "ms_per_step": round(R2["ms_per_step"], 3),
+                "tokens_per_s": round(S2["T"] / (R2["ms_per_step"] * 1e-3), 1),
+                "kernel_ms": {k: round(v, 3) for k, v in R2["kernel_ms"].items()},
+                "pi_frac_of_bf16_peak": round(R2["pi_frac"], 4), "mu_frac_of_fp8_peak": round(R2["mu_frac"], 4),
+                "mfma_frac_combined": round(R2["mfma_frac_combined"], 4)}
+            del S2
+            torch.cuda.empty_cache()
+        log("workloads:", line["workloads"])
     print(json.dumps(line), flush=True)
 
 
@@ -349,7 +382,7 @@ def library_leg(torch, w, T, H, W, hq, hs, wq, ws, pi_ms, mu_ms, reps=2):
     return res if reps else None
 
 
-def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, score_ms, reps=2):
+def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, packed, score_ms, reps=2):
     """The scoring call with the full-vocabulary measures (KL both ways,
     Euclidean distance) switched on: both score kernels also store their
     logits (4 B each) for passes of 16384 rows and a streaming kernel reads
@@ -360,7 +393,7 @@ def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, score_ms
     def run():
         return acrl.acrl_score_pi_mu(H, W, hq, hs, wq, ws, w.scaling, ids, inv_temperature=w.inv_temperature,
                                      out_slot=slots, n_slots=w.slots, outputs=outs, want=("entropy",),
-                                     divergence=True)
+                                     divergence=True, packed_weights=packed)
 
     outs.update(run())
     torch.cuda.synchronize()

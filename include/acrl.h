@@ -35,7 +35,7 @@
 extern "C" {
 #endif
 
-#define ACRL_ABI_VERSION 5
+#define ACRL_ABI_VERSION 6
 
 typedef int acrl_status;
 enum {
@@ -74,6 +74,13 @@ typedef enum {
   ACRL_CTRL_CONTINUOUS = 3,   /* Sec. 5 ablation "continuous reduction": alpha = -k sign(A)    */
   ACRL_CTRL_FALLBACK = 4      /* Sec. 5 ablation "fallback to GRPO": weight 1 when Y < X       */
 } acrl_ctrl_mode;
+
+/* Which policies one acrl_score_pi_mu call scores (acrl_score_desc.policies). */
+enum {
+  ACRL_POLICY_BOTH = 0,       /* pi and mu (the default)                            */
+  ACRL_POLICY_PI = 1,         /* pi only: the mu operands and outputs are not read   */
+  ACRL_POLICY_MU = 2          /* mu only: the pi operands and outputs are not read   */
+};
 
 /* Slots of the batch statistics vector (double[ACRL_N_STATS]). */
 enum {
@@ -149,7 +156,12 @@ acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, vo
  * given, becomes nonzero; the flag is never cleared by the library).
  * The workspace holds a tiled copy of W, h, Wq and hq and of the E8M0 scales
  * of Wq and hq (about (3 + 1/32) (V + n_rows) d bytes) besides the per-strip
- * partial states.
+ * partial states; with packed_weights (acrl_pack_weights) the copies of W and
+ * Wq come from there and the workspace holds only the activations'
+ * (acrl_score_workspace_query).
+ * policies = ACRL_POLICY_PI scores pi only (h, w, logp_pi required; the mu
+ * fields are not read and the mu outputs not written), ACRL_POLICY_MU mu only;
+ * the full-vocabulary measures need both.
  *
  * Full-vocabulary measures (optional; the paper's measure is the absolute
  * distance on the sampled token, Eq. distance_metric, and it names the KL
@@ -192,10 +204,17 @@ typedef struct acrl_score_desc {
   float* kl_mu_pi;              /* [slots] out, nullable: KL(mu || pi)                       */
   float* l2;                    /* [slots] out, nullable: Euclidean distance of p and q      */
   int64_t div_chunk;            /* rows per pass of the three measures (0 = 16384)           */
+  int32_t policies;             /* ACRL_POLICY_*: both (0), pi only or mu only               */
+  const void* packed_weights;   /* nullable: W and Wq as acrl_pack_weights laid them out     */
+  size_t packed_weights_bytes;  /* acrl_packed_weights_size() bytes when packed_weights set   */
 } acrl_score_desc;
 
 acrl_status acrl_score_workspace_size(int64_t n_rows, int64_t d, int64_t V, int mu_scaling,
                                       size_t* bytes);
+/* Workspace of the call the descriptor describes (reads n_rows, d, V,
+ * mu_scaling, the full-vocabulary outputs, div_chunk and whether
+ * packed_weights is set; the pointers are not dereferenced).              */
+acrl_status acrl_score_workspace_query(const acrl_score_desc* desc, size_t* bytes);
 /* Workspace of a call that also asks for the full-vocabulary measures.      */
 acrl_status acrl_score_div_workspace_size(int64_t n_rows, int64_t d, int64_t V, int mu_scaling,
                                           int64_t div_chunk, size_t* bytes);
@@ -213,7 +232,9 @@ acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream);
  * log mu(a_r).  The draw depends only on (seed, row_offset + r), so chunked
  * calls reproduce one call.
  * Requirements: as acrl_score_pi_mu for n_rows, d, V, mu_scaling and the
- * operands; workspace of acrl_score_workspace_size() bytes.
+ * operands; workspace of acrl_score_workspace_size() bytes (with
+ * packed_weights, what acrl_score_workspace_query gives for a descriptor with
+ * the same sizes and packed_weights set suffices).
  */
 typedef struct acrl_sample_desc {
   int64_t n_rows;
@@ -231,17 +252,27 @@ typedef struct acrl_sample_desc {
   float* logp_mu;               /* [n_rows] out, nullable                                   */
   void* workspace;
   size_t workspace_bytes;
+  const void* packed_weights;   /* nullable: from acrl_pack_weights (W's part is not read)   */
+  size_t packed_weights_bytes;
 } acrl_sample_desc;
 
 acrl_status acrl_sample_mu(const acrl_sample_desc* desc, void* stream);
 
-/* Tracing hook (observability, per calling thread).  With n == 4, every later
- * acrl_score_pi_mu call of this thread records the caller-owned hipEvent_t
- * handles events[0..3] on its stream: before the pi kernel, between the pi and
- * mu kernels, between the mu kernel and the merge, and after the merge, so
- * the caller can time each kernel.  n == 0 (events may be NULL) turns it off.
- * The event handles must stay valid while tracing is on.                    */
-acrl_status acrl_trace_score_events(void* const* events, int n);
+/* Packed LM head (once per weight version).  The scorers stream their
+ * operands from a tiled copy: per 256-row tile and 64-byte K chunk, one
+ * contiguous 16 KiB image of the tile's rows, each row's four 16-byte pieces
+ * at positions c ^ ((row / 4) mod 4), rows past V repeating row V-1; for MX32
+ * also the E8M0 scales of Wq per tile and chunk.  acrl_pack_weights writes
+ * that copy of W and Wq (and Wq's MX scales) into caller-owned device memory
+ * of acrl_packed_weights_size() bytes; passing it as packed_weights to
+ * acrl_score_pi_mu / acrl_sample_mu skips their own packing of W and Wq, so
+ * the per-step calls pack only the activations.  Valid as long as W, Wq and
+ * their scales do not change (the weights of theta_old are quantized once
+ * per weight version, Sec. 5.1).  w, wq, wq_scales: as acrl_score_pi_mu's;
+ * same requirements on V, d and the alignment.                              */
+acrl_status acrl_packed_weights_size(int64_t V, int64_t d, int mu_scaling, size_t* bytes);
+acrl_status acrl_pack_weights(const void* w, const void* wq, const void* wq_scales, int64_t V, int64_t d,
+                              int mu_scaling, void* packed, size_t packed_bytes, void* stream);
 
 /* ======================================================================== */
 /* a6/a7  acrl_discrepancy_reduce -- per-token d, segmented reductions       */

@@ -22,6 +22,7 @@ SCALE_PER_TENSOR, SCALE_PER_ROW, SCALE_MX32 = 0, 1, 2
 ROUND_NEAREST_EVEN, ROUND_TOWARD_ZERO = 0, 1
 Y_GROUP, Y_SEQUENCE, Y_BATCH = 0, 1, 2
 CTRL_ACRL, CTRL_TIS, CTRL_MIS, CTRL_CONTINUOUS, CTRL_FALLBACK = 0, 1, 2, 3, 4
+POLICY_BOTH, POLICY_PI, POLICY_MU = 0, 1, 2
 N_STATS = 10
 STAT_NAMES = ["y_batch", "tok_mean_d", "tok_max_d", "tok_std_d", "mean_h_pi", "mean_h_mu",
               "n_tokens", "n_groups", "tok_mean_logratio", "n_seqs"]
@@ -29,7 +30,8 @@ STAT_NAMES = ["y_batch", "tok_mean_d", "tok_max_d", "tok_std_d", "mean_h_pi", "m
 EXPORTED = [
     "acrl_status_string", "acrl_last_error", "acrl_abi_version", "acrl_abi_struct_sizes",
     "acrl_quantize_workspace_size", "acrl_quantize_fp8", "acrl_fp8_encode",
-    "acrl_score_workspace_size", "acrl_score_div_workspace_size", "acrl_score_pi_mu", "acrl_trace_score_events",
+    "acrl_score_workspace_size", "acrl_score_div_workspace_size", "acrl_score_workspace_query", "acrl_score_pi_mu",
+    "acrl_packed_weights_size", "acrl_pack_weights",
     "acrl_reduce_workspace_size", "acrl_discrepancy_reduce", "acrl_discrepancy_reduce_noalloc",
     "acrl_controller_step", "acrl_reference_from_groups", "acrl_sample_mu",
     "acrl_surrogate_workspace_size", "acrl_surrogate",
@@ -51,7 +53,8 @@ class ScoreDesc(ctypes.Structure):
                 ("logp_pi", _P), ("logp_mu", _P), ("entropy_pi", _P), ("entropy_mu", _P),
                 ("lse_pi", _P), ("lse_mu", _P), ("logit_pi", _P), ("logit_mu", _P),
                 ("error_flag", _P), ("workspace", _P), ("workspace_bytes", _SZ),
-                ("kl_pi_mu", _P), ("kl_mu_pi", _P), ("l2", _P), ("div_chunk", _I64)]
+                ("kl_pi_mu", _P), ("kl_mu_pi", _P), ("l2", _P), ("div_chunk", _I64),
+                ("policies", _I32), ("packed_weights", _P), ("packed_weights_bytes", _SZ)]
 
 
 class ReduceDesc(ctypes.Structure):
@@ -92,7 +95,8 @@ class SampleDesc(ctypes.Structure):
                 ("hq", _P), ("hq_scales", _P), ("wq", _P), ("wq_scales", _P),
                 ("mu_scaling", _I32), ("inv_temperature", _F32),
                 ("seed", ctypes.c_uint64), ("row_offset", _I64),
-                ("ids", _P), ("logp_mu", _P), ("workspace", _P), ("workspace_bytes", _SZ)]
+                ("ids", _P), ("logp_mu", _P), ("workspace", _P), ("workspace_bytes", _SZ),
+                ("packed_weights", _P), ("packed_weights_bytes", _SZ)]
 
 
 class AcrlError(RuntimeError):
@@ -134,8 +138,12 @@ def lib() -> ctypes.CDLL:
         L.acrl_score_div_workspace_size.argtypes = [_I64, _I64, _I64, _I32, _I64, ctypes.POINTER(_SZ)]
         L.acrl_score_pi_mu.restype = _I32
         L.acrl_score_pi_mu.argtypes = [ctypes.POINTER(ScoreDesc), _P]
-        L.acrl_trace_score_events.restype = _I32
-        L.acrl_trace_score_events.argtypes = [ctypes.POINTER(_P), _I32]
+        L.acrl_score_workspace_query.restype = _I32
+        L.acrl_score_workspace_query.argtypes = [ctypes.POINTER(ScoreDesc), ctypes.POINTER(_SZ)]
+        L.acrl_packed_weights_size.restype = _I32
+        L.acrl_packed_weights_size.argtypes = [_I64, _I64, _I32, ctypes.POINTER(_SZ)]
+        L.acrl_pack_weights.restype = _I32
+        L.acrl_pack_weights.argtypes = [_P, _P, _P, _I64, _I64, _I32, _P, _SZ, _P]
         L.acrl_reduce_workspace_size.restype = _I32
         L.acrl_reduce_workspace_size.argtypes = [_I64, _I64, _I64, ctypes.POINTER(_SZ)]
         L.acrl_discrepancy_reduce.restype = _I32
@@ -255,16 +263,35 @@ def acrl_fp8_encode(x: torch.Tensor, rounding: int = ROUND_NEAREST_EVEN, q=None,
 
 
 # ------------------------------------------------------------------ a3..a5
+def acrl_pack_weights(w, wq, wq_scales, mu_scaling: int, packed=None, stream=None):
+    """The tiled copy of W and Wq (and Wq's MX scales) the scorers stream
+    from, once per weight version; returns the uint8 device buffer to pass
+    as packed_weights."""
+    _dev(w, torch.bfloat16, "w")
+    _dev(wq, torch.uint8, "wq")
+    V, d = w.shape
+    nb = _SZ()
+    _check(lib().acrl_packed_weights_size(V, d, mu_scaling, ctypes.byref(nb)), "acrl_packed_weights_size")
+    if packed is None:
+        packed = torch.empty(nb.value, dtype=torch.uint8, device=w.device)
+    _check(lib().acrl_pack_weights(_ptr(w), _ptr(wq), _ptr(wq_scales), V, d, mu_scaling, _ptr(packed),
+                                   packed.numel(), _stream(stream)), "acrl_pack_weights")
+    return packed
+
+
 def acrl_score_pi_mu(h, w, hq, hq_scales, wq, wq_scales, mu_scaling: int, token_ids,
                      inv_temperature: float = 1.0, mask=None, out_slot=None, n_slots=None,
                      outputs: Optional[dict] = None, want=("entropy", "lse", "logit"),
-                     error_flag=None, stream=None, divergence: bool = False, div_chunk: int = 0) -> dict:
+                     error_flag=None, stream=None, divergence: bool = False, div_chunk: int = 0,
+                     policies: int = POLICY_BOTH, packed_weights=None) -> dict:
     """Score every row of h under pi (bf16) and mu (fp8/mxfp8).
 
     Returns a dict of float32 [n_slots] tensors: logp_pi, logp_mu and, per
     `want`, entropy_pi/mu, lse_pi/mu, logit_pi/mu; with divergence=True also
     the full-vocabulary kl_pi_mu, kl_mu_pi and l2.  Pass `outputs` to reuse
-    preallocated tensors."""
+    preallocated tensors.  policies = POLICY_PI / POLICY_MU scores one
+    policy only (the other's outputs are left untouched); packed_weights is
+    the buffer acrl_pack_weights returned for these w, wq."""
     _dev(h, torch.bfloat16, "h")
     _dev(w, torch.bfloat16, "w")
     _dev(hq, torch.uint8, "hq")
@@ -284,14 +311,6 @@ def acrl_score_pi_mu(h, w, hq, hq_scales, wq, wq_scales, mu_scaling: int, token_
     for k in names:
         if k not in out:
             out[k] = torch.zeros(n_slots, dtype=torch.float32, device=dev)
-    nb = _SZ()
-    if divergence:
-        _check(lib().acrl_score_div_workspace_size(n_rows, d, V, mu_scaling, int(div_chunk), ctypes.byref(nb)),
-               "acrl_score_div_workspace_size")
-    else:
-        _check(lib().acrl_score_workspace_size(n_rows, d, V, mu_scaling, ctypes.byref(nb)),
-               "acrl_score_workspace_size")
-    ws = _workspace(nb.value, dev, stream)
     desc = ScoreDesc(n_rows=n_rows, d=d, V=V, h=_ptr(h), w=_ptr(w), hq=_ptr(hq),
                      hq_scales=_ptr(hq_scales), wq=_ptr(wq), wq_scales=_ptr(wq_scales),
                      mu_scaling=mu_scaling, inv_temperature=float(inv_temperature),
@@ -300,17 +319,23 @@ def acrl_score_pi_mu(h, w, hq, hq_scales, wq, wq_scales, mu_scaling: int, token_
                      entropy_pi=_ptr(out.get("entropy_pi")), entropy_mu=_ptr(out.get("entropy_mu")),
                      lse_pi=_ptr(out.get("lse_pi")), lse_mu=_ptr(out.get("lse_mu")),
                      logit_pi=_ptr(out.get("logit_pi")), logit_mu=_ptr(out.get("logit_mu")),
-                     error_flag=_ptr(error_flag), workspace=_ptr(ws), workspace_bytes=nb.value,
+                     error_flag=_ptr(error_flag),
                      kl_pi_mu=_ptr(out.get("kl_pi_mu") if divergence else None),
                      kl_mu_pi=_ptr(out.get("kl_mu_pi") if divergence else None),
-                     l2=_ptr(out.get("l2") if divergence else None), div_chunk=int(div_chunk))
+                     l2=_ptr(out.get("l2") if divergence else None), div_chunk=int(div_chunk),
+                     policies=int(policies), packed_weights=_ptr(packed_weights),
+                     packed_weights_bytes=0 if packed_weights is None else packed_weights.numel())
+    nb = _SZ()
+    _check(lib().acrl_score_workspace_query(ctypes.byref(desc), ctypes.byref(nb)), "acrl_score_workspace_query")
+    ws = _workspace(nb.value, dev, stream)
+    desc.workspace, desc.workspace_bytes = _ptr(ws), nb.value
     _check(lib().acrl_score_pi_mu(ctypes.byref(desc), _stream(stream)), "acrl_score_pi_mu")
     return out
 
 
 def acrl_sample_mu(hq, hq_scales, wq, wq_scales, mu_scaling: int, seed: int, row_offset: int = 0,
                    inv_temperature: float = 1.0, ids=None, logp_mu=None, want_logp: bool = True,
-                   stream=None):
+                   stream=None, packed_weights=None):
     """Draw one token per row of hq from mu (Gumbel-max in the mu kernel).
 
     Returns (ids int32 [n_rows], logp_mu float32 [n_rows] or None)."""
@@ -324,26 +349,17 @@ def acrl_sample_mu(hq, hq_scales, wq, wq_scales, mu_scaling: int, seed: int, row
     if logp_mu is None and want_logp:
         logp_mu = torch.empty(n_rows, dtype=torch.float32, device=dev)
     nb = _SZ()
-    _check(lib().acrl_score_workspace_size(n_rows, d, V, mu_scaling, ctypes.byref(nb)),
-           "acrl_score_workspace_size")
+    probe = ScoreDesc(n_rows=n_rows, d=d, V=V, mu_scaling=mu_scaling, packed_weights=_ptr(packed_weights))
+    _check(lib().acrl_score_workspace_query(ctypes.byref(probe), ctypes.byref(nb)), "acrl_score_workspace_query")
     ws = _workspace(nb.value, dev, stream)
     desc = SampleDesc(n_rows=n_rows, d=d, V=V, hq=_ptr(hq), hq_scales=_ptr(hq_scales), wq=_ptr(wq),
                       wq_scales=_ptr(wq_scales), mu_scaling=mu_scaling,
                       inv_temperature=float(inv_temperature), seed=int(seed) & (2 ** 64 - 1),
                       row_offset=int(row_offset), ids=_ptr(ids), logp_mu=_ptr(logp_mu),
-                      workspace=_ptr(ws), workspace_bytes=nb.value)
+                      workspace=_ptr(ws), workspace_bytes=nb.value, packed_weights=_ptr(packed_weights),
+                      packed_weights_bytes=0 if packed_weights is None else packed_weights.numel())
     _check(lib().acrl_sample_mu(ctypes.byref(desc), _stream(stream)), "acrl_sample_mu")
     return ids, logp_mu
-
-
-def acrl_trace_score_events(events) -> None:
-    """events: four torch.cuda.Event (already recorded once, so they exist)
-    or None to stop tracing."""
-    if events is None:
-        _check(lib().acrl_trace_score_events(None, 0), "acrl_trace_score_events")
-        return
-    arr = (_P * 4)(*[e.cuda_event for e in events])
-    _check(lib().acrl_trace_score_events(arr, 4), "acrl_trace_score_events")
 
 
 # ------------------------------------------------------------------ a6/a7

@@ -39,11 +39,18 @@ struct ScorePlan {
   size_t ws_zbuf_offset[2];  //   the logits of pi and mu of one pass
   size_t ws_bytes;
 };
-// div_rows > 0 plans the full-vocabulary measures in passes of div_rows rows.
-ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows = 0);
+// div_rows > 0 plans the full-vocabulary measures in passes of div_rows rows;
+// prepacked: W's and Wq's images come from the caller (no workspace for them).
+ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows = 0, bool prepacked = false);
 constexpr int64_t kDivergenceChunk = 16384;  // default rows per pass of the full-vocabulary measures
-// Events recorded around the score kernels (tracing hook), per thread.
-void set_score_trace(void* const* events, int n);
+// Caller-owned packed LM head (acrl_pack_weights): byte offsets of the W,
+// Wq and Wq-MX-scale images.
+struct PackedWeightsLayout {
+  size_t w_offset, wq_offset, mx_offset, bytes;
+};
+PackedWeightsLayout packed_weights_layout(int64_t V, int64_t d, int mu_scaling);
+hipError_t launch_pack_weights(const void* w, const void* wq, const void* wq_scales, int64_t V, int64_t d,
+                               int mu_scaling, void* packed, hipStream_t s);
 hipError_t launch_score(const acrl_score_desc& desc, const ScorePlan& plan, hipStream_t s);
 hipError_t launch_sample(const acrl_sample_desc& desc, const ScorePlan& plan, hipStream_t s);
 

@@ -93,16 +93,43 @@ acrl_status validate_score(const acrl_score_desc* d) {
                "mu_scaling %d unknown", d->mu_scaling);
   ACRL_REQUIRE(d->inv_temperature > 0.0f && d->inv_temperature < 1e30f,
                "inv_temperature must be positive and finite");
-  ACRL_REQUIRE(d->w && d->wq && d->wq_scales, "w, wq and wq_scales are required");
-  ACRL_REQUIRE(aligned16(d->w) && aligned16(d->wq) && aligned16(d->wq_scales),
-               "w, wq, wq_scales must be 16-byte aligned");
+  ACRL_REQUIRE(d->policies == ACRL_POLICY_BOTH || d->policies == ACRL_POLICY_PI || d->policies == ACRL_POLICY_MU,
+               "policies %d unknown", d->policies);
+  const bool pi = d->policies != ACRL_POLICY_MU, mu = d->policies != ACRL_POLICY_PI;
+  const bool div = d->kl_pi_mu || d->kl_mu_pi || d->l2;
+  ACRL_REQUIRE(!div || (pi && mu), "the full-vocabulary measures need both policies");
+  if (d->packed_weights) {
+    const size_t need = packed_weights_layout(d->V, d->d, d->mu_scaling).bytes;
+    ACRL_REQUIRE(d->packed_weights_bytes >= need, "packed_weights has %zu bytes, needs %zu",
+                 d->packed_weights_bytes, need);
+    ACRL_REQUIRE(aligned16(d->packed_weights), "packed_weights must be 16-byte aligned");
+  }
+  if (pi && !d->packed_weights) {
+    ACRL_REQUIRE(d->w, "w is required");
+    ACRL_REQUIRE(aligned16(d->w), "w must be 16-byte aligned");
+  }
+  if (mu) {
+    ACRL_REQUIRE(d->wq_scales && (d->wq || d->packed_weights), "wq and wq_scales are required");
+    ACRL_REQUIRE(aligned16(d->wq) && aligned16(d->wq_scales), "wq, wq_scales must be 16-byte aligned");
+  }
   if (d->n_rows > 0) {
-    ACRL_REQUIRE(d->h && d->hq && d->hq_scales && d->token_ids && d->logp_pi && d->logp_mu,
-                 "h, hq, hq_scales, token_ids, logp_pi and logp_mu are required");
-    ACRL_REQUIRE(aligned16(d->h) && aligned16(d->hq) && aligned16(d->hq_scales),
-                 "h, hq, hq_scales must be 16-byte aligned");
+    ACRL_REQUIRE(d->token_ids, "token_ids is required");
+    if (pi) {
+      ACRL_REQUIRE(d->h && d->logp_pi, "h and logp_pi are required");
+      ACRL_REQUIRE(aligned16(d->h), "h must be 16-byte aligned");
+    }
+    if (mu) {
+      ACRL_REQUIRE(d->hq && d->hq_scales && d->logp_mu, "hq, hq_scales and logp_mu are required");
+      ACRL_REQUIRE(aligned16(d->hq) && aligned16(d->hq_scales), "hq, hq_scales must be 16-byte aligned");
+    }
   }
   return ACRL_OK;
+}
+
+// rows per pass of the full-vocabulary measures (0: not asked for)
+int64_t div_rows_of(const acrl_score_desc* d) {
+  const bool div = d->kl_pi_mu || d->kl_mu_pi || d->l2;
+  return div ? (d->div_chunk > 0 ? d->div_chunk : kDivergenceChunk) : 0;
 }
 
 acrl_status validate_reduce(const acrl_reduce_desc* d) {
@@ -223,13 +250,50 @@ acrl_status acrl_score_div_workspace_size(int64_t n_rows, int64_t d, int64_t V, 
   return ACRL_OK;
 }
 
+acrl_status acrl_score_workspace_query(const acrl_score_desc* desc, size_t* bytes) {
+  ACRL_REQUIRE(desc && bytes, "desc and bytes are required");
+  acrl_status st = acrl_score_workspace_size(desc->n_rows, desc->d, desc->V, desc->mu_scaling, bytes);
+  if (st != ACRL_OK) return st;
+  ACRL_REQUIRE(desc->div_chunk >= 0 && desc->div_chunk <= ((int64_t)1 << 24), "div_chunk must lie in [0, 2^24]");
+  *bytes = acrl::plan_score(desc->n_rows, desc->d, desc->V, acrl::div_rows_of(desc), desc->packed_weights != nullptr)
+               .ws_bytes;
+  return ACRL_OK;
+}
+
+acrl_status acrl_packed_weights_size(int64_t V, int64_t d, int mu_scaling, size_t* bytes) {
+  ACRL_REQUIRE(bytes, "bytes is NULL");
+  ACRL_REQUIRE(d > 0 && d % 128 == 0, "d must be a positive multiple of 128");
+  ACRL_REQUIRE(V > 0 && V < (int64_t)INT32_MAX - 512, "V out of range");
+  ACRL_REQUIRE(mu_scaling >= ACRL_SCALE_PER_TENSOR && mu_scaling <= ACRL_SCALE_MX32, "mu_scaling unknown");
+  ACRL_REQUIRE(acrl::score_size_ok(V, d), "V x d too large");
+  *bytes = acrl::packed_weights_layout(V, d, mu_scaling).bytes;
+  return ACRL_OK;
+}
+
+acrl_status acrl_pack_weights(const void* w, const void* wq, const void* wq_scales, int64_t V, int64_t d,
+                              int mu_scaling, void* packed, size_t packed_bytes, void* stream) {
+  size_t need = 0;
+  acrl_status st = acrl_packed_weights_size(V, d, mu_scaling, &need);
+  if (st != ACRL_OK) return st;
+  ACRL_REQUIRE(w && wq && wq_scales && packed, "w, wq, wq_scales and packed are required");
+  ACRL_REQUIRE(acrl::aligned16(w) && acrl::aligned16(wq) && acrl::aligned16(wq_scales) && acrl::aligned16(packed),
+               "w, wq, wq_scales and packed must be 16-byte aligned");
+  if (packed_bytes < need) {
+    set_error("acrl_pack_weights needs %zu bytes, got %zu", need, packed_bytes);
+    return ACRL_ERR_WORKSPACE;
+  }
+  st = acrl::check_device();
+  if (st != ACRL_OK) return st;
+  return acrl::hip_status(acrl::launch_pack_weights(w, wq, wq_scales, V, d, mu_scaling, packed, (hipStream_t)stream),
+                          "acrl_pack_weights launch");
+}
+
 acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream) {
   acrl_status st = acrl::validate_score(desc);
   if (st != ACRL_OK) return st;
-  const bool div = desc->kl_pi_mu || desc->kl_mu_pi || desc->l2;
   ACRL_REQUIRE(desc->div_chunk >= 0 && desc->div_chunk <= ((int64_t)1 << 24), "div_chunk must lie in [0, 2^24]");
-  const acrl::ScorePlan plan = acrl::plan_score(
-      desc->n_rows, desc->d, desc->V, div ? (desc->div_chunk > 0 ? desc->div_chunk : acrl::kDivergenceChunk) : 0);
+  const acrl::ScorePlan plan = acrl::plan_score(desc->n_rows, desc->d, desc->V, acrl::div_rows_of(desc),
+                                                desc->packed_weights != nullptr);
   if (desc->n_rows > 0 && (!desc->workspace || desc->workspace_bytes < plan.ws_bytes)) {
     set_error("acrl_score_pi_mu needs %zu workspace bytes, got %zu", plan.ws_bytes, desc->workspace_bytes);
     return ACRL_ERR_WORKSPACE;
@@ -257,13 +321,19 @@ acrl_status acrl_sample_mu(const acrl_sample_desc* d, void* stream) {
                "inv_temperature must be positive and finite");
   ACRL_REQUIRE(d->row_offset >= 0 && d->row_offset + d->n_rows <= ((int64_t)1 << 32),
                "row_offset + n_rows must lie in [0, 2^32] (the generator's token counter)");
-  ACRL_REQUIRE(d->wq && d->wq_scales, "wq and wq_scales are required");
+  ACRL_REQUIRE(d->wq_scales && (d->wq || d->packed_weights), "wq and wq_scales are required");
   ACRL_REQUIRE(acrl::aligned16(d->wq) && acrl::aligned16(d->wq_scales), "wq and wq_scales must be 16-byte aligned");
+  if (d->packed_weights) {
+    const size_t need = acrl::packed_weights_layout(d->V, d->d, d->mu_scaling).bytes;
+    ACRL_REQUIRE(d->packed_weights_bytes >= need, "packed_weights has %zu bytes, needs %zu",
+                 d->packed_weights_bytes, need);
+    ACRL_REQUIRE(acrl::aligned16(d->packed_weights), "packed_weights must be 16-byte aligned");
+  }
   if (d->n_rows > 0) {
     ACRL_REQUIRE(d->hq && d->hq_scales && d->ids, "hq, hq_scales and ids are required");
     ACRL_REQUIRE(acrl::aligned16(d->hq) && acrl::aligned16(d->hq_scales), "hq and hq_scales must be 16-byte aligned");
   }
-  const acrl::ScorePlan plan = acrl::plan_score(d->n_rows, d->d, d->V);
+  const acrl::ScorePlan plan = acrl::plan_score(d->n_rows, d->d, d->V, 0, d->packed_weights != nullptr);
   if (d->n_rows > 0 && (!d->workspace || d->workspace_bytes < plan.ws_bytes)) {
     set_error("acrl_sample_mu needs %zu workspace bytes, got %zu", plan.ws_bytes, d->workspace_bytes);
     return ACRL_ERR_WORKSPACE;
@@ -275,16 +345,6 @@ acrl_status acrl_sample_mu(const acrl_sample_desc* d, void* stream) {
   acrl_status st = acrl::check_device();
   if (st != ACRL_OK) return st;
   return acrl::hip_status(acrl::launch_sample(*d, plan, (hipStream_t)stream), "acrl_sample_mu launch");
-}
-
-acrl_status acrl_trace_score_events(void* const* events, int n) {
-  ACRL_REQUIRE(n == 0 || n == 4, "n must be 0 or 4");
-  if (n == 4) {
-    ACRL_REQUIRE(events, "events is NULL");
-    for (int k = 0; k < 4; ++k) ACRL_REQUIRE(events[k], "events[%d] is NULL", k);
-  }
-  acrl::set_score_trace(events, n);
-  return ACRL_OK;
 }
 
 acrl_status acrl_reduce_workspace_size(int64_t B, int64_t L, int64_t n_groups, size_t* bytes) {

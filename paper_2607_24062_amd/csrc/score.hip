@@ -1141,9 +1141,10 @@ struct MergeParams {
   float* lse[2];
   float* zout[2];
   int32_t* error_flag;
+  int q_begin, q_end;      // policies merged: [q_begin, q_end) of {pi, mu}
 };
 
-// One thread per row: combine the strips' states of pi and mu.
+// One thread per row: combine the strips' states of pi and / or mu.
 __global__ __launch_bounds__(256) void merge_kernel(MergeParams p) {
   const int r = blockIdx.x * blockDim.x + threadIdx.x;
   if (r >= p.n_rows) return;
@@ -1153,8 +1154,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeParams p) {
   const bool id_ok = id >= 0 && id < p.V;
   if (active && !id_ok && p.error_flag) atomicOr(p.error_flag, 1);
   const int64_t plane = (int64_t)p.n_strips * p.n_rows;
-#pragma unroll
-  for (int q = 0; q < 2; ++q) {
+  for (int q = p.q_begin; q < p.q_end; ++q) {
     float lse = 0.f, ent = 0.f, lp = 0.f, z = 0.f;
     if (active) {
       float M = kInitMax, S = 0.f, U = 0.f;
@@ -1213,21 +1213,37 @@ __global__ __launch_bounds__(256) void sample_merge_kernel(SampleMergeParams p) 
 
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-thread_local hipEvent_t g_trace[4];
-thread_local bool g_trace_on = false;
-
-inline void trace(int k, hipStream_t s) {
-  if (g_trace_on) (void)hipEventRecord(g_trace[k], s);
-}
-
 }  // namespace
 
-void set_score_trace(void* const* events, int n) {
-  g_trace_on = n == 4;
-  for (int k = 0; k < 4; ++k) g_trace[k] = g_trace_on ? (hipEvent_t)events[k] : nullptr;
+PackedWeightsLayout packed_weights_layout(int64_t V, int64_t d, int mu_scaling) {
+  PackedWeightsLayout l{};
+  const size_t vrows = (size_t)((V + kTileV - 1) / kTileV) * kTileV;
+  l.w_offset = 0;
+  l.wq_offset = align_up(vrows * 2 * (size_t)d, 256);
+  l.mx_offset = l.wq_offset + align_up(vrows * (size_t)d, 256);
+  l.bytes = l.mx_offset + (mu_scaling == ACRL_SCALE_MX32 ? align_up(vrows * (size_t)(d / 32), 256) : 0);
+  return l;
 }
 
-ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows) {
+hipError_t launch_pack_weights(const void* w, const void* wq, const void* wq_scales, int64_t V, int64_t d,
+                               int mu_scaling, void* packed, hipStream_t s) {
+  const PackedWeightsLayout l = packed_weights_layout(V, d, mu_scaling);
+  uint8_t* dst = static_cast<uint8_t*>(packed);
+  const int64_t n_vtiles = (V + kTileV - 1) / kTileV;
+  const void* srcs[2] = {w, wq};
+  const size_t offs[2] = {l.w_offset, l.wq_offset};
+  for (int q = 0; q < 2; ++q) {
+    const int64_t row_bytes = q == 0 ? 2 * d : d;
+    const int64_t units = n_vtiles * kTileV * (row_bytes / 16);
+    const unsigned blocks = (unsigned)std::min<int64_t>((units + 255) / 256, 8192);
+    hipLaunchKernelGGL(pack_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint8_t*>(srcs[q]),
+                       (uint32_t)V, (uint32_t)row_bytes, (uint32_t)units, dst + offs[q]);
+  }
+  if (mu_scaling == ACRL_SCALE_MX32) launch_pack_mx(wq_scales, V, d, n_vtiles, dst + l.mx_offset, s);
+  return hipGetLastError();
+}
+
+ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows, bool prepacked) {
   ScorePlan pl{};
   pl.n_ttiles = (int)((n_rows + kTileT - 1) / kTileT);
   pl.n_vtiles = (int)((V + kTileV - 1) / kTileV);
@@ -1281,18 +1297,20 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows) {
   // sampling: the strips' best Gumbel key, its logit and row
   pl.ws_best_offset = off;
   off += 3 * align_up((size_t)pl.n_strips * (size_t)n_rows * sizeof(float), 256);
-  // packed operands: W, H (2d bytes per row), Wq, Hq (d bytes per row)
+  // packed operands: W, H (2d bytes per row), Wq, Hq (d bytes per row);
+  // the weight images (W, Wq and Wq's MX scales) only when they do not come
+  // prepacked by the caller
   const size_t vrows = (size_t)pl.n_vtiles * kTileV, trows = (size_t)pl.n_ttiles * kTileT;
   const size_t pack_bytes[4] = {vrows * 2 * (size_t)d, trows * 2 * (size_t)d, vrows * (size_t)d, trows * (size_t)d};
   for (int q = 0; q < 4; ++q) {
     pl.ws_pack_offset[q] = off;
-    off += align_up(pack_bytes[q], 256);
+    if (!(prepacked && (q == 0 || q == 2))) off += align_up(pack_bytes[q], 256);
   }
   // MX: packed E8M0 scale images of Wq and Hq (d/32 bytes per row)
   const size_t mx_bytes[2] = {vrows * (size_t)(d / 32), trows * (size_t)(d / 32)};
   for (int q = 0; q < 2; ++q) {
     pl.ws_mx_offset[q] = off;
-    off += align_up(mx_bytes[q], 256);
+    if (!(prepacked && q == 0)) off += align_up(mx_bytes[q], 256);
   }
   // full-vocabulary measures: the logits of both policies for one pass of
   // div_tiles token tiles, row-major with the padded vocabulary as stride
@@ -1328,11 +1346,19 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   pp.ids = dsc.token_ids;
   pp.mx_row_bytes = (int)(dsc.d / 32);
 
-  // operands -> packed images in the workspace
+  const bool do_pi = dsc.policies != ACRL_POLICY_MU;
+  const bool do_mu = dsc.policies != ACRL_POLICY_PI;
+  const uint8_t* pw = static_cast<const uint8_t*>(dsc.packed_weights);
+  const PackedWeightsLayout pwl = packed_weights_layout(dsc.V, dsc.d, dsc.mu_scaling);
+
+  // operands -> packed images in the workspace (the weight images only when
+  // the caller did not pass them prepacked)
   const void* srcs[4] = {dsc.w, dsc.h, dsc.wq, dsc.hq};
   const int64_t src_rows[4] = {dsc.V, dsc.n_rows, dsc.V, dsc.n_rows};
   const int64_t src_tiles[4] = {pl.n_vtiles, pl.n_ttiles, pl.n_vtiles, pl.n_ttiles};
   for (int q = 0; q < 4; ++q) {
+    if (!(q < 2 ? do_pi : do_mu)) continue;
+    if (pw && (q == 0 || q == 2)) continue;
     const int64_t row_bytes = q < 2 ? 2 * dsc.d : dsc.d;
     const int64_t units = src_tiles[q] * kTileV * (row_bytes / 16);
     const unsigned blocks = (unsigned)std::min<int64_t>((units + 255) / 256, 8192);
@@ -1341,7 +1367,7 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   }
 
   // pi: bf16 operands
-  pp.a = ws + pl.ws_pack_offset[0];
+  pp.a = pw ? pw + pwl.w_offset : ws + pl.ws_pack_offset[0];
   pp.b = ws + pl.ws_pack_offset[1];
   pp.n_chunks = (int)(2 * dsc.d / kChunk);
   pp.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[0]);
@@ -1349,15 +1375,15 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
 
   // mu: e4m3 operands
   ScoreParams pm = pp;
-  pm.a = ws + pl.ws_pack_offset[2];
+  pm.a = pw ? pw + pwl.wq_offset : ws + pl.ws_pack_offset[2];
   pm.b = ws + pl.ws_pack_offset[3];
   pm.n_chunks = (int)(dsc.d / kChunk);
   pm.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[1]);
   pm.logit = reinterpret_cast<float*>(ws + pl.ws_logit_offset[1]);
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
-    launch_pack_mx(dsc.wq_scales, dsc.V, dsc.d, pl.n_vtiles, ws + pl.ws_mx_offset[0], s);
-    launch_pack_mx(dsc.hq_scales, dsc.n_rows, dsc.d, pl.n_ttiles, ws + pl.ws_mx_offset[1], s);
-    pm.a_mx = ws + pl.ws_mx_offset[0];
+    if (do_mu && !pw) launch_pack_mx(dsc.wq_scales, dsc.V, dsc.d, pl.n_vtiles, ws + pl.ws_mx_offset[0], s);
+    if (do_mu) launch_pack_mx(dsc.hq_scales, dsc.n_rows, dsc.d, pl.n_ttiles, ws + pl.ws_mx_offset[1], s);
+    pm.a_mx = pw ? pw + pwl.mx_offset : ws + pl.ws_mx_offset[0];
     pm.b_mx = ws + pl.ws_mx_offset[1];
   } else {
     pm.a_scale = static_cast<const float*>(dsc.wq_scales);
@@ -1372,12 +1398,10 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
     else
       launch_score_kernel<kFP8Tensor, E>(g, q, s);
   };
-  const bool div = dsc.kl_pi_mu || dsc.kl_mu_pi || dsc.l2;
-  trace(0, s);
+  const bool div = dsc.kl_pi_mu || dsc.kl_mu_pi || dsc.l2;  // both policies (checked by the caller)
   if (!div) {
-    launch_score_kernel<kBF16, kEpiSoftmax>(grid, pp, s);
-    trace(1, s);
-    launch_mu(pm, grid, std::integral_constant<int, kEpiSoftmax>{});
+    if (do_pi) launch_score_kernel<kBF16, kEpiSoftmax>(grid, pp, s);
+    if (do_mu) launch_mu(pm, grid, std::integral_constant<int, kEpiSoftmax>{});
   } else {
     // passes of div_tiles token tiles: pi and mu (softmax + the logits
     // stored), then the measures of the pass's rows
@@ -1420,10 +1444,8 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
       const int rows = (int)std::min<int64_t>(dsc.n_rows - dp.r0, (int64_t)nt * kTileT);
       hipLaunchKernelGGL(divergence_kernel, dim3((unsigned)rows), dim3(256), 0, s, dp);
     }
-    trace(1, s);
   }
 
-  trace(2, s);
   MergeParams mp{};
   mp.n_rows = (int)dsc.n_rows;
   mp.n_strips = pl.n_strips;
@@ -1440,8 +1462,9 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   mp.lse[0] = dsc.lse_pi;         mp.lse[1] = dsc.lse_mu;
   mp.zout[0] = dsc.logit_pi;      mp.zout[1] = dsc.logit_mu;
   mp.error_flag = dsc.error_flag;
+  mp.q_begin = do_pi ? 0 : 1;
+  mp.q_end = do_mu ? 2 : 1;
   hipLaunchKernelGGL(merge_kernel, dim3((unsigned)((dsc.n_rows + 255) / 256)), dim3(256), 0, s, mp);
-  trace(3, s);
   return hipGetLastError();
 }
 
@@ -1590,10 +1613,13 @@ hipError_t launch_backward(const acrl_backward_desc& dsc, const BackwardPlan& pl
 hipError_t launch_sample(const acrl_sample_desc& dsc, const ScorePlan& pl, hipStream_t s) {
   if (dsc.n_rows == 0) return hipSuccess;
   uint8_t* ws = static_cast<uint8_t*>(dsc.workspace);
+  const uint8_t* pw = static_cast<const uint8_t*>(dsc.packed_weights);
+  const PackedWeightsLayout pwl = packed_weights_layout(dsc.V, dsc.d, dsc.mu_scaling);
   const void* srcs[2] = {dsc.wq, dsc.hq};
   const int64_t src_rows[2] = {dsc.V, dsc.n_rows};
   const int64_t src_tiles[2] = {pl.n_vtiles, pl.n_ttiles};
   for (int q = 0; q < 2; ++q) {
+    if (q == 0 && pw) continue;  // Wq comes prepacked
     const int64_t units = src_tiles[q] * kTileV * (dsc.d / 16);
     const unsigned blocks = (unsigned)std::min<int64_t>((units + 255) / 256, 8192);
     hipLaunchKernelGGL(pack_kernel, dim3(blocks), dim3(256), 0, s, static_cast<const uint8_t*>(srcs[q]),
@@ -1609,7 +1635,7 @@ hipError_t launch_sample(const acrl_sample_desc& dsc, const ScorePlan& pl, hipSt
   pm.n_tblocks = pl.n_tblocks;
   pm.inv_temp = dsc.inv_temperature;
   pm.mx_row_bytes = (int)(dsc.d / 32);
-  pm.a = ws + pl.ws_pack_offset[2];
+  pm.a = pw ? pw + pwl.wq_offset : ws + pl.ws_pack_offset[2];
   pm.b = ws + pl.ws_pack_offset[3];
   pm.n_chunks = (int)(dsc.d / kChunk);
   pm.part = reinterpret_cast<float*>(ws + pl.ws_part_offset[1]);
@@ -1622,9 +1648,9 @@ hipError_t launch_sample(const acrl_sample_desc& dsc, const ScorePlan& pl, hipSt
   pm.best_id = reinterpret_cast<int32_t*>(ws + pl.ws_best_offset + 2 * best_plane);
   const unsigned grid = (unsigned)pl.grid;
   if (dsc.mu_scaling == ACRL_SCALE_MX32) {
-    launch_pack_mx(dsc.wq_scales, dsc.V, dsc.d, pl.n_vtiles, ws + pl.ws_mx_offset[0], s);
+    if (!pw) launch_pack_mx(dsc.wq_scales, dsc.V, dsc.d, pl.n_vtiles, ws + pl.ws_mx_offset[0], s);
     launch_pack_mx(dsc.hq_scales, dsc.n_rows, dsc.d, pl.n_ttiles, ws + pl.ws_mx_offset[1], s);
-    pm.a_mx = ws + pl.ws_mx_offset[0];
+    pm.a_mx = pw ? pw + pwl.mx_offset : ws + pl.ws_mx_offset[0];
     pm.b_mx = ws + pl.ws_mx_offset[1];
     launch_score_kernel<kMX, kEpiSample>(grid, pm, s);
   } else {

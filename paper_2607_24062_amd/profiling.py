@@ -14,6 +14,7 @@ dispatch, are scaled by what they read for that copy.
 Command line:
     python -m paper_2607_24062_amd.profiling stats CSV TITLE COMMAND > profiles/x.md
     python -m paper_2607_24062_amd.profiling traffic FETCH_CSV WRITE_CSV TITLE COMMAND > profiles/y.md
+    python -m paper_2607_24062_amd.profiling trace TRACE_CSV TITLE COMMAND [PREFIX] > profiles/z.md
 """
 from __future__ import annotations
 
@@ -141,8 +142,16 @@ def mfma_markdown(counter_csv: str, trace_csv: str, title: str, commands: str) -
             d = cnt.setdefault(short_name(r["Kernel_Name"]), {})
             d.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
     dur = {}
-    with open(trace_csv) as f:
+    # durations from the kernel trace, or (trace_csv "-") from the counter
+    # pass's own per-dispatch timestamps
+    src = counter_csv if trace_csv == "-" else trace_csv
+    seen = set()
+    with open(src) as f:
         for r in csv.DictReader(f):
+            key = (r.get("Dispatch_Id"), r["Kernel_Name"])
+            if trace_csv == "-" and key in seen:
+                continue
+            seen.add(key)
             dur.setdefault(short_name(r["Kernel_Name"]), []).append(
                 (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
     lines = ["# " + title, "", "Commands (from the repository root on one MI355X):", "", "```", commands, "```", "",
@@ -192,7 +201,34 @@ def per_cu_markdown(counter_csv: str, title: str, command: str) -> str:
     return "\n".join(lines) + "\n"
 
 
+def trace_rows(trace_csv: str, prefix: str = ""):
+    """Per (kernel, launch size) from a --kernel-trace CSV: calls, mean,
+    min and max duration (ms), for the kernels whose short name starts with
+    `prefix`.  One launch size per workload and call shape, so the rows keep
+    the workloads of one run apart."""
+    acc = {}
+    with open(trace_csv) as f:
+        for r in csv.DictReader(f):
+            k = short_name(r["Kernel_Name"])
+            if not k.startswith(prefix):
+                continue
+            wg = int(r["Grid_Size_X"]) // max(int(r["Workgroup_Size_X"]), 1)
+            acc.setdefault((k, wg), []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-6)
+    return [(k, wg, len(v), sum(v) / len(v), min(v), max(v)) for (k, wg), v in acc.items()]
+
+
+def trace_markdown(trace_csv: str, title: str, command: str, prefix: str = "") -> str:
+    out = ["# %s" % title, "", "Command (from the repository root on one MI355X):", "", "```", command, "```", "",
+           "| kernel | workgroups | calls | average ms | min ms | max ms |", "|---|---|---|---|---|---|"]
+    for k, wg, n, a, lo, hi in sorted(trace_rows(trace_csv, prefix), key=lambda r: -r[2] * r[3]):
+        out.append("| %s | %d | %d | %.4f | %.4f | %.4f |" % (k, wg, n, a, lo, hi))
+    return "\n".join(out) + "\n"
+
+
 def main(argv):
+    if len(argv) >= 4 and argv[0] == "trace":
+        sys.stdout.write(trace_markdown(argv[1], argv[2], argv[3], argv[4] if len(argv) > 4 else ""))
+        return 0
     if len(argv) >= 4 and argv[0] == "percu":
         sys.stdout.write(per_cu_markdown(argv[1], argv[2], argv[3]))
         return 0

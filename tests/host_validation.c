@@ -67,6 +67,25 @@ int main(void) {
   expect("score div_chunk", acrl_score_pi_mu(&sd, NULL), ACRL_ERR_INVALID_ARG);
   sd.div_chunk = 0; sd.V = (int64_t)1 << 40;
   expect("score V", acrl_score_pi_mu(&sd, NULL), ACRL_ERR_INVALID_ARG);
+  sd.V = 1000; sd.l2 = NULL;
+  /* policies, packed weights, descriptor workspace query */
+  sd.policies = 7;
+  expect("score policies", acrl_score_pi_mu(&sd, NULL), ACRL_ERR_INVALID_ARG);
+  sd.policies = ACRL_POLICY_PI; sd.l2 = (float*)p;
+  expect("score div one policy", acrl_score_pi_mu(&sd, NULL), ACRL_ERR_INVALID_ARG);
+  sd.l2 = NULL; sd.policies = ACRL_POLICY_MU; sd.hq = NULL;
+  expect("score mu hq", acrl_score_pi_mu(&sd, NULL), ACRL_ERR_INVALID_ARG);
+  sd.hq = p; sd.policies = ACRL_POLICY_BOTH; sd.packed_weights = p; sd.packed_weights_bytes = 16;
+  expect("score packed bytes", acrl_score_pi_mu(&sd, NULL), ACRL_ERR_INVALID_ARG);
+  size_t nb2 = 0, nb3 = 0;
+  expect("score ws query desc packed", acrl_score_workspace_query(&sd, &nb2), ACRL_OK);
+  sd.packed_weights = NULL;
+  expect("score ws query desc", acrl_score_workspace_query(&sd, &nb3), ACRL_OK);
+  if (!(nb2 < nb3)) ++failures;
+  expect("packed size", acrl_packed_weights_size(1000, 256, 2, &nb2), ACRL_OK);
+  expect("packed size d", acrl_packed_weights_size(1000, 100, 2, &nb2), ACRL_ERR_INVALID_ARG);
+  expect("pack null", acrl_pack_weights(NULL, p, p, 1000, 256, 1, p, (size_t)1 << 30, NULL), ACRL_ERR_INVALID_ARG);
+  expect("pack bytes", acrl_pack_weights(p, p, p, 1000, 256, 1, p, 16, NULL), ACRL_ERR_WORKSPACE);
   expect("score ws query", acrl_score_workspace_size(300, 256, 1000, 1, &nb), ACRL_OK);
   expect("score div ws query", acrl_score_div_workspace_size(300, 256, 1000, 1, 0, &nb), ACRL_OK);
   expect("score ws d", acrl_score_workspace_size(300, 100, 1000, 1, &nb), ACRL_ERR_INVALID_ARG);
@@ -129,9 +148,7 @@ int main(void) {
   expect("backward ws query", acrl_backward_workspace_size(300, 256, 1000, 0, &nb), ACRL_OK);
   expect("backward ws chunk", acrl_backward_workspace_size(300, 256, 1000, -1, &nb), ACRL_ERR_INVALID_ARG);
 
-  /* tracing hook, host helper */
-  expect("trace n", acrl_trace_score_events(NULL, 3), ACRL_ERR_INVALID_ARG);
-  expect("trace off", acrl_trace_score_events(NULL, 0), ACRL_OK);
+  /* host helper */
   const float gy[3] = {0.01f, 0.5f, 0.03f};
   const int32_t gn[3] = {8, 0, 8};
   float X = 0.0f;

@@ -58,7 +58,7 @@ def test_descriptor_layout_matches_binding():
     assert [s.value for s in sizes] == [ctypes.sizeof(acrl.ScoreDesc), ctypes.sizeof(acrl.ReduceDesc),
                                         ctypes.sizeof(acrl.ControllerDesc), ctypes.sizeof(acrl.SampleDesc),
                                         ctypes.sizeof(acrl.SurrogateDesc), ctypes.sizeof(acrl.BackwardDesc)]
-    assert acrl.lib().acrl_abi_version() == 5
+    assert acrl.lib().acrl_abi_version() == 6
 
 
 def test_status_strings():

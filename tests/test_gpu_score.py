@@ -325,3 +325,41 @@ def test_truncated_fp8_end_to_end(scaling):
     res = {k: down(v) for k, v in out.items()}
     ref = oracle.score(H, W, hq_o, hs_o, wq_o, ws_o, scaling, ids)
     _compare(res, ref, V)
+
+
+@pytest.mark.parametrize("scaling", [oracle.PER_ROW, oracle.PER_TENSOR, oracle.MX32])
+def test_packed_weights_and_single_policy_calls(scaling):
+    # W and Wq packed once (acrl_pack_weights) give the same bits as the
+    # call that packs them itself; pi-only and mu-only calls give the fused
+    # call's bits and leave the other policy's outputs untouched; the sampler
+    # draws the same ids from the packed Wq
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    T, V, d = 700, 1500, 256
+    H = random_bf16((T, d), 81)
+    W = random_bf16((V, d), 82, std=2.5 / 16)
+    h, w = up_bf16(torch, dev, H), up_bf16(torch, dev, W)
+    hq, hs = acrl.acrl_quantize_fp8(h, scaling)
+    wq, ws = acrl.acrl_quantize_fp8(w, scaling)
+    ids = up(torch, dev, np.random.default_rng(83).integers(0, V, size=T).astype(np.int32))
+    packed = acrl.acrl_pack_weights(w, wq, ws, scaling)
+    base = acrl.acrl_score_pi_mu(h, w, hq, hs, wq, ws, scaling, ids)
+    pk = acrl.acrl_score_pi_mu(h, w, hq, hs, wq, ws, scaling, ids, packed_weights=packed)
+    keys = list(base)
+    sentinel = lambda: {k: torch.full((T,), 7.0, device=dev) for k in keys}
+    pi_only = acrl.acrl_score_pi_mu(h, w, hq, hs, wq, ws, scaling, ids, policies=acrl.POLICY_PI,
+                                    packed_weights=packed, outputs=sentinel())
+    mu_only = acrl.acrl_score_pi_mu(h, w, hq, hs, wq, ws, scaling, ids, policies=acrl.POLICY_MU,
+                                    outputs=sentinel())
+    s0, _ = acrl.acrl_sample_mu(hq, hs, wq, ws, scaling, 5)
+    s1, _ = acrl.acrl_sample_mu(hq, hs, wq, ws, scaling, 5, packed_weights=packed)
+    torch.cuda.synchronize()
+    for k in keys:
+        assert np.array_equal(down(pk[k]), down(base[k])), k
+        if k.endswith("_pi"):
+            assert np.array_equal(down(pi_only[k]), down(base[k])), k
+            assert np.all(down(mu_only[k]) == 7.0), k
+        else:
+            assert np.array_equal(down(mu_only[k]), down(base[k])), k
+            assert np.all(down(pi_only[k]) == 7.0), k
+    assert np.array_equal(down(s0), down(s1))
