@@ -223,14 +223,25 @@ acrl_status acrl_score_pi_mu(const acrl_score_desc* desc, void* stream);
 /* ======================================================================== */
 /* Sampling from mu (the step before scoring: the rollout's token draw)      */
 /* ======================================================================== *
- * For every row r: a_r = argmax_v [ z_v - ln(-ln u_v) ] with z the mu logits
- * (as in acrl_score_pi_mu, 1/tau applied) and u_v = (w >> 9 + 1/2) 2^-23,
- * w = word (v mod 4) of Philox4x32-10 (Salmon et al., SC 2011) on counter
- * (v / 4, row_offset + r, 0, 0) under key (seed low, seed high 32 bits): the
- * Gumbel-max trick, i.e. a draw from softmax(z), fused into the mu kernel's
- * epilogue (the logits never reach memory).  logp_mu[r] (nullable) =
- * log mu(a_r).  The draw depends only on (seed, row_offset + r), so chunked
- * calls reproduce one call.
+ For every row r, a draw a_r from softmax(z), with z the mu logits (as in
+ * acrl_score_pi_mu, 1/tau applied), by blockwise Gumbel-max.  The vocabulary
+ * is cut into blocks of 16 rows: row v lies in block k = 2 floor(v/32) +
+ * (floor(v/4) mod 2).  The step runs in three parts.
+ *  1. Each block gets one key, lse_k - ln(-ln u_k), with lse_k the
+ *     log-sum-exp of its logits.
+ *  2. The block of the largest key wins.
+ *  3. Inside the winning block, a_r is the first row (in increasing v) whose
+ *     cumulative softmax probability within the block exceeds u'_k.
+ * This is exactly a draw from softmax(z): the maximum of z_v + Gumbel over a
+ * block is lse_k + Gumbel, and the row attaining it has probability
+ * exp(z_v - lse_k), independently.  u_k and u'_k are words 2e and 2e+1,
+ * with e = floor(k/2) mod 2, of Philox4x32-10 (Salmon et al., SC 2011) on
+ * counter (floor(v/64), row_offset + r, k mod 2, 0) under key (seed low,
+ * seed high 32 bits), as (w >> 9 + 1/2) 2^-23.  The draw is fused into the
+ * mu kernel's epilogue: the logits never reach memory, and one generator
+ * call serves 32 logits.  logp_mu[r] (nullable) = log mu(a_r).  The draw
+ * depends only on (seed, row_offset + r), so chunked calls reproduce one
+ * call.
  * Requirements: as acrl_score_pi_mu for n_rows, d, V, mu_scaling and the
  * operands; workspace of acrl_score_workspace_size() bytes (with
  * packed_weights, what acrl_score_workspace_query gives for a descriptor with

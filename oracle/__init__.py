@@ -96,6 +96,12 @@ def lib() -> ctypes.CDLL:
         L.acrl_ref_philox4x32_10.argtypes = [P, P, P]
         L.acrl_ref_sample_uniform.restype = D
         L.acrl_ref_sample_uniform.argtypes = [ctypes.c_uint64, I64, I64]
+        L.acrl_ref_block_gumbel_sample.restype = I32
+        L.acrl_ref_block_gumbel_sample.argtypes = [P, I64, I64, ctypes.c_uint64, I64, P, P, P]
+        L.acrl_ref_block_gumbel_keys.restype = I32
+        L.acrl_ref_block_gumbel_keys.argtypes = [P, I64, ctypes.c_uint64, I64, P]
+        L.acrl_ref_block_pick.restype = I64
+        L.acrl_ref_block_pick.argtypes = [P, I64, ctypes.c_uint64, I64, I64, P, P]
         L.acrl_ref_gumbel_sample.restype = I32
         L.acrl_ref_gumbel_sample.argtypes = [P, I64, I64, ctypes.c_uint64, I64, P, P]
         L.acrl_ref_reference_x.restype = I32
@@ -337,6 +343,49 @@ def gumbel_sample(z: np.ndarray, seed: int, row_offset: int = 0):
     _check(lib().acrl_ref_gumbel_sample(_p(z), n_rows, V, seed, row_offset, _p(ids), _p(keys)),
            "gumbel_sample")
     return ids, keys
+
+
+def block_gumbel_sample(z: np.ndarray, seed: int, row_offset: int = 0):
+    """Blockwise Gumbel-max draw from softmax(z) per row (two uniforms per
+    16-row block); returns (ids, winning keys, winning blocks)."""
+    z = _c(z, np.float64)
+    n_rows, V = z.shape
+    ids = np.empty(n_rows, np.int32)
+    keys = np.empty(n_rows)
+    blocks = np.empty(n_rows, np.int64)
+    _check(lib().acrl_ref_block_gumbel_sample(_p(z), n_rows, V, seed, row_offset, _p(ids), _p(keys), _p(blocks)),
+           "block_gumbel_sample")
+    return ids, keys, blocks
+
+
+def block_gumbel_keys(z_row: np.ndarray, seed: int, t: int) -> np.ndarray:
+    """Every block's key lse_k - ln(-ln u_k) of one token's logits."""
+    z = _c(z_row, np.float64)
+    keys = np.empty(2 * ((z.size + 31) // 32))
+    _check(lib().acrl_ref_block_gumbel_keys(_p(z), z.size, seed, t, _p(keys)), "block_gumbel_keys")
+    return keys
+
+
+def block_pick(z_row: np.ndarray, seed: int, t: int, k: int):
+    """(row, cumulative probabilities of the block's 16 slots, u'_k)."""
+    z = _c(z_row, np.float64)
+    cum = np.empty(16)
+    u = np.empty(1)
+    row = lib().acrl_ref_block_pick(_p(z), z.size, seed, t, int(k), _p(cum), _p(u))
+    return int(row), cum, float(u[0])
+
+
+def block_slot_rows(k: int, V: int) -> np.ndarray:
+    """Rows of block k's 16 slots (-1 past V), in slot order."""
+    q = np.arange(16)
+    v = 32 * (k // 2) + 8 * (q // 4) + 4 * (k % 2) + q % 4
+    return np.where(v < V, v, -1)
+
+
+def block_of_row(v):
+    """Block of vocabulary row v in the blockwise sampler."""
+    v = np.asarray(v, np.int64)
+    return 2 * (v // 32) + (v // 4) % 2
 
 
 # ------------------------------------------------- surrogate and backward

@@ -636,6 +636,136 @@ int acrl_ref_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t 
   return 0;
 }
 
+/* Blockwise Gumbel-max: the same draw from softmax(z) with two uniforms per
+ * block of vocabulary rows instead of one per row.  The vocabulary is cut
+ * into blocks of 16 rows: row v lies in block k(v) = 2 floor(v/32) +
+ * (floor(v/4) mod 2), i.e. block k holds rows 32 floor(k/2) + 8q + 4 (k mod 2)
+ * + j, q, j in 0..3 (fewer at the end of the vocabulary).  Two facts make it
+ * exact.  First, the largest of z_v + G_v over a block is distributed as
+ * lse_k + G with one Gumbel G (the Gumbel family is max-stable).  Second,
+ * which row attains it is independent of that value and has probability
+ * exp(z_v - lse_k).  So the block is drawn by Gumbel-max over the keys
+ * lse_k - ln(-ln u_k), and the row inside it by inverse CDF with a second
+ * uniform u'_k.
+ * Uniforms: Philox4x32-10 on counter (floor(v/64), row_offset + r,
+ * k mod 2, 0) under key (seed low, seed high); e = floor(k/2) mod 2 picks
+ * words 2e (u_k) and 2e+1 (u'_k); u = (w >> 9 + 1/2) 2^-23.  Ties between
+ * block keys go to the smaller block; inside the block the first row (in
+ * increasing v) whose cumulative probability exceeds u'_k, else the block's
+ * last row of nonzero probability. */
+static void block_uniforms(uint64_t seed, int64_t t, int64_t k, double* u_key, double* u_pick) {
+  const int64_t v0 = 32 * (k / 2) + 4 * (k % 2); /* first row of block k */
+  const uint32_t ctr[4] = {(uint32_t)(v0 / 64), (uint32_t)t, (uint32_t)(k % 2), 0u};
+  const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+  uint32_t w[4];
+  acrl_ref_philox4x32_10(ctr, key, w);
+  const int e = (int)((k / 2) % 2);
+  *u_key = ((double)(w[2 * e] >> 9) + 0.5) / 8388608.0;
+  *u_pick = ((double)(w[2 * e + 1] >> 9) + 0.5) / 8388608.0;
+}
+
+/* Row of slot q (0..15) of block k, or -1 past the vocabulary. */
+static int64_t block_row(int64_t k, int q, int64_t V) {
+  const int64_t v = 32 * (k / 2) + 8 * (q / 4) + 4 * (k % 2) + (q % 4);
+  return v < V ? v : -1;
+}
+
+/* Key of every block of one token's logits zr (n_blocks = 2 ceil(V/32)):
+ * lse of the block's rows - ln(-ln u_k); -inf for a block past V. */
+int acrl_ref_block_gumbel_keys(const double* zr, int64_t V, uint64_t seed, int64_t t, double* keys) {
+  if (!zr || !keys || V <= 0) return -1;
+  const int64_t n_blocks = 2 * ((V + 31) / 32);
+  for (int64_t k = 0; k < n_blocks; ++k) {
+    double m = -INFINITY;
+    for (int q = 0; q < 16; ++q) {
+      const int64_t v = block_row(k, q, V);
+      if (v >= 0 && zr[v] > m) m = zr[v];
+    }
+    if (m == -INFINITY) {
+      keys[k] = -INFINITY;
+      continue;
+    }
+    double sum = 0.0;
+    for (int q = 0; q < 16; ++q) {
+      const int64_t v = block_row(k, q, V);
+      if (v >= 0) sum += exp(zr[v] - m);
+    }
+    double u_key, u_pick;
+    block_uniforms(seed, t, k, &u_key, &u_pick);
+    keys[k] = m + log(sum) - log(-log(u_key));
+  }
+  return 0;
+}
+
+/* The row block k gives token t: the first row (in increasing v) whose
+ * cumulative softmax probability within the block exceeds u'_k, else the
+ * block's last row of nonzero probability.  cum (nullable, 16 entries): the
+ * cumulative probabilities after each slot (NaN past V); u_pick (nullable):
+ * u'_k. */
+int64_t acrl_ref_block_pick(const double* zr, int64_t V, uint64_t seed, int64_t t, int64_t k, double* cum,
+                            double* u_pick_out) {
+  double u_key, u_pick;
+  block_uniforms(seed, t, k, &u_key, &u_pick);
+  double m = -INFINITY;
+  for (int q = 0; q < 16; ++q) {
+    const int64_t v = block_row(k, q, V);
+    if (v >= 0 && zr[v] > m) m = zr[v];
+  }
+  double total = 0.0;
+  int64_t last = -1;
+  for (int q = 0; q < 16; ++q) {
+    const int64_t v = block_row(k, q, V);
+    if (v < 0) continue;
+    const double e = exp(zr[v] - m);
+    total += e;
+    if (e > 0.0) last = v;
+  }
+  int64_t pick = last;
+  int found = 0;
+  double c = 0.0;
+  for (int q = 0; q < 16; ++q) {
+    const int64_t v = block_row(k, q, V);
+    if (v < 0) {
+      if (cum) cum[q] = NAN;
+      continue;
+    }
+    c += exp(zr[v] - m);
+    if (cum) cum[q] = c / total;
+    if (!found && c > u_pick * total) {
+      pick = v;
+      found = 1;
+    }
+  }
+  if (u_pick_out) *u_pick_out = u_pick;
+  return pick;
+}
+
+int acrl_ref_block_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t seed,
+                                 int64_t row_offset, int32_t* ids, double* key_out,
+                                 int64_t* block_out) {
+  if (!z || !ids || V <= 0 || n_rows < 0) return -1;
+  const int64_t n_blocks = 2 * ((V + 31) / 32);
+  double* keys = (double*)malloc((size_t)n_blocks * sizeof(double));
+  if (!keys) return -1;
+  for (int64_t r = 0; r < n_rows; ++r) {
+    const double* zr = z + r * V;
+    acrl_ref_block_gumbel_keys(zr, V, seed, row_offset + r, keys);
+    /* the block of the largest key (the smaller block on a tie) */
+    double best = -INFINITY;
+    int64_t best_k = -1;
+    for (int64_t k = 0; k < n_blocks; ++k)
+      if (keys[k] > best) {
+        best = keys[k];
+        best_k = k;
+      }
+    ids[r] = (int32_t)acrl_ref_block_pick(zr, V, seed, row_offset + r, best_k, NULL, NULL);
+    if (key_out) key_out[r] = best;
+    if (block_out) block_out[r] = best_k;
+  }
+  free(keys);
+  return 0;
+}
+
 /* ------------------------------------------------------------------ */
 /* The ACRL-weighted surrogate (Eq. ACRL) and its LM-head backward      */
 /* ------------------------------------------------------------------ */

@@ -180,6 +180,20 @@ int acrl_ref_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t 
 /* ---- fixture helper (not part of the method): inverse-CDF sampling ----- *
  * Samples one id per row from softmax(z_row) using the supplied uniform
  * u[r] in [0,1): the smallest v whose cumulative probability exceeds u.     */
+/* Blockwise Gumbel-max: blocks of 16 vocabulary rows (row v in block
+ * 2 floor(v/32) + (floor(v/4) mod 2)); one Gumbel key lse_k - ln(-ln u_k)
+ * per block, then the row inside the winning block by inverse CDF with
+ * u'_k; u_k, u'_k from Philox4x32-10 on (floor(v/64), row_offset + r,
+ * k mod 2, 0), words 2e and 2e+1 with e = floor(k/2) mod 2.  A draw from
+ * softmax(z).  key_out / block_out (nullable): the winning key and block. */
+int acrl_ref_block_gumbel_sample(const double* z, int64_t n_rows, int64_t V, uint64_t seed,
+                                 int64_t row_offset, int32_t* ids, double* key_out,
+                                 int64_t* block_out);
+/* The pieces of it: every block's key for token t, and the row block k
+ * gives (cum: its 16 cumulative probabilities, u_pick: u'_k; nullable). */
+int acrl_ref_block_gumbel_keys(const double* zr, int64_t V, uint64_t seed, int64_t t, double* keys);
+int64_t acrl_ref_block_pick(const double* zr, int64_t V, uint64_t seed, int64_t t, int64_t k, double* cum,
+                            double* u_pick_out);
 int acrl_ref_sample_inverse_cdf(const double* z, int64_t n_rows, int64_t V,
                                 const double* u, int32_t* ids);
 

@@ -517,6 +517,8 @@ void score_kernel(ScoreParams p) {
     // (rows past V present) takes its own copy of the code.
     auto run = [&](auto tail_tag) {
       constexpr bool kTail = decltype(tail_tag)::value;
+      uint32_t pw[JT][2];  // sampling: the Philox words the odd block of a pair uses
+      (void)pw;
 #pragma unroll
       for (int b = 0; b < 4; ++b) {
 #pragma unroll
@@ -603,32 +605,67 @@ void score_kernel(ScoreParams p) {
           // pass is sunk past it and the values of all 16 blocks stay live
           asm volatile("" : "+v"(M[j]), "+v"(S[j]), "+v"(U[j]));
           if constexpr (SAMPLE) {
-            // Gumbel-max: key = y - log2(-log2 u), a monotone map of
-            // z - ln(-ln u); u from Philox on counter (v / 4, token, 0, 0),
-            // one call per 4 consecutive rows
+            // Blockwise Gumbel-max.  The lane's 16 rows v0 + 32b + 8q + 4g + jj
+            // (in increasing order) are one block k = 2 (v0 + 32b) / 32 + g
+            // of the draw: its key is the block's log-sum-exp plus one
+            // Gumbel, lse2 - log2(-log2 u) in log2 units (a monotone map of
+            // lse - ln(-ln u)), lse2 = M + log2 of the block's share of S
+            // (sh[0], relative to the running maximum M just set).  Only a
+            // block that beats the lane's best so far draws its row: inverse
+            // CDF of the block's softmax with the second uniform.  Uniforms:
+            // Philox on counter ((v0 + 32b) / 64, token, g, 0), words 2e and
+            // 2e + 1 for e = b mod 2, so one call serves the blocks of b and
+            // b + 1 (the second pair is kept in pw).
             const uint32_t tokg = (uint32_t)(p.row_offset + tok[j]);
-#pragma unroll
-            for (int q4 = 0; q4 < 4; ++q4) {
-              const int vb = v0 + 32 * b + 8 * q4 + 4 * g;  // multiple of 4
+            uint32_t wk, wp;
+            if (b % 2 == 0) {
               uint32_t w4[4];
-              philox4x32_10((uint32_t)vb >> 2, tokg, 0u, 0u, p.seed_lo, p.seed_hi, w4);
+              philox4x32_10((uint32_t)(v0 + 32 * b) >> 6, tokg, (uint32_t)g, 0u, p.seed_lo, p.seed_hi, w4);
+              wk = w4[0];
+              wp = w4[1];
+              pw[j][0] = w4[2];
+              pw[j][1] = w4[3];
+            } else {
+              wk = pw[j][0];
+              wp = pw[j][1];
+            }
+            const float u = ((float)(wk >> 9) + 0.5f) * 0x1p-23f;
+            const float key = M[j] + __builtin_amdgcn_logf(sh[0]) - __builtin_amdgcn_logf(-__builtin_amdgcn_logf(u));
+            if (key > bk[j]) {
+              // the block's row: the first whose cumulative weight exceeds
+              // u' times the block's total (in row order), else its last row
+              // of nonzero weight; weights 2^(y - M) as in the sums above
+              const float up = ((float)(wp >> 9) + 0.5f) * 0x1p-23f;
+              // two passes over the weights (recomputed: fewer live registers)
+              auto weight = [&](int i) {
+                float e = fast_exp2(fmaf(v[i], c2[j], -M[j]));
+                if constexpr (kTail) e *= fminf(fmaxf(nv - (float)(16 * b + i), 0.0f), 1.0f);
+                return e;
+              };
+              float tot = 0.0f;
 #pragma unroll
-              for (int ii = 0; ii < 4; ++ii) {
-                const int i = 4 * q4 + ii;
-                // the logit again from its accumulator (scaled as above):
-                // fewer values live across the generator calls
-                float vi = acc_read(acc[b][j][i]);
-                if constexpr (MODE == kFP8Row) vi *= rs[i];
-                const float u = ((float)(w4[ii] >> 9) + 0.5f) * 0x1p-23f;
-                float key = fmaf(vi, c2[j], -__builtin_amdgcn_logf(-__builtin_amdgcn_logf(u)));
-                if constexpr (kTail) key = (nv - (float)(16 * b + i)) > 0.0f ? key : -INFINITY;
-                if (key > bk[j]) {
-                  bk[j] = key;
-                  bz[j] = vi * cz[j];
-                  bi[j] = vb + ii;
-                }
+              for (int i = 0; i < 16; ++i) tot += weight(i);
+              const float target = up * tot;
+              float c = 0.0f, zsel = 0.0f, zlast = 0.0f;
+              int isel = -1, ilast = 0;
+#pragma unroll
+              for (int i = 0; i < 16; ++i) {
+                const float ei = weight(i);
+                c += ei;
+                const bool hit = isel < 0 && c > target;
+                isel = hit ? i : isel;
+                zsel = hit ? v[i] : zsel;
+                const bool pos = ei > 0.0f;
+                ilast = pos ? i : ilast;
+                zlast = pos ? v[i] : zlast;
               }
-              __builtin_amdgcn_sched_barrier(0);  // one generator call live at a time
+              if (isel < 0) {
+                isel = ilast;
+                zsel = zlast;
+              }
+              bk[j] = key;
+              bz[j] = zsel * cz[j];
+              bi[j] = v0 + 32 * b + 8 * (isel >> 2) + 4 * g + (isel & 3);
             }
           }
           // the sampled token a_t: rare branch, taken by the one lane holding it
@@ -935,13 +972,13 @@ void score_kernel(ScoreParams p) {
 
 // Waves per workgroup of each instantiation (measured on the MI355X): two
 // per SIMD where the variant runs faster that way (the per-row FP8 scorer
-// spills 40 bytes per lane at 8 waves and is still 5-7 % faster; the
-// sampling variants spill at either width, far less at 8, and run ~20 %
-// faster there); one per SIMD otherwise.
+// spills 40 bytes per lane at 8 waves and is still 5-7 % faster); one per
+// SIMD otherwise.  The blockwise sampling variants fit their registers at 4
+// waves (no spills) and run as fast or faster there than at 8 (q8b 85.2 vs
+// 85.4 ms, q17b 27.0 vs 30.6 ms), where they spill around the epilogue.
 template <int MODE, int EPI>
 constexpr int waves_for() {
-  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) || (EPI == kEpiSoftmaxZ && MODE == kBF16) ||
-          (EPI == kEpiSample && MODE != kMX))
+  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) || (EPI == kEpiSoftmaxZ && MODE == kBF16))
              ? 8
              : 4;
 }

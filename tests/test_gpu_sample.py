@@ -1,13 +1,17 @@
-"""GPU parity of acrl_sample_mu (Gumbel-max draw from mu, fused into the mu
-kernel) with the oracle's Gumbel-max sampler on the same counter-based
-uniforms (Philox4x32-10).
+"""GPU parity of acrl_sample_mu (blockwise Gumbel-max draw from mu, fused
+into the mu kernel) with the oracle's blockwise sampler on the same
+counter-based uniforms (Philox4x32-10).
 
-Where floating point decides the argmax, the kernel's fp32 logits and
-hardware log2 may pick a different row than the oracle's fp64 keys when the
-two best keys are within rounding: the drawn row must then be within that
-rounding of the oracle's best key, and rows whose best key clears the
-runner-up by more than it must match exactly.  The sampled log-prob is
-checked like the scorer's (2e-3)."""
+The draw has two steps.  First a block of 16 vocabulary rows wins by
+Gumbel-max over the blocks' keys.  Then the row inside it comes from the
+inverse CDF of the block's softmax.  Floating point decides both steps.
+The kernel uses fp32 logits and the hardware log2; the oracle uses fp64.
+The kernel's block must have a key within rounding of the oracle's best
+key; where the oracle's best block clears the runner-up by more than
+that, the blocks must match.  The row must be the oracle's pick in that
+block, unless u' falls within rounding of a cumulative-probability
+boundary; then it must be a row whose interval touches u'.  The sampled
+log-prob is checked like the scorer's (2e-3)."""
 import numpy as np
 import pytest
 
@@ -19,16 +23,33 @@ from gpu_util import down, torch_dev, up, up_bf16
 pytestmark = pytest.mark.gpu
 
 KEY_TOL = 2e-3  # fp32 logits (~1e-5 relative) and the hardware log2 against fp64
+CUM_TOL = 1e-4  # fp32 exponentials and running sums of 16 weights
 
 
-def _oracle_keys(z, seed, row_offset):
+def _check_draw(z, ids, seed, row_offset):
     n, V = z.shape
-    u = np.array([[oracle.sample_uniform(seed, row_offset + r, v) for v in range(V)] for r in range(n)])
-    return z - np.log(-np.log(u))
+    n_clear = 0
+    for r in range(n):
+        t = row_offset + r
+        keys = oracle.block_gumbel_keys(z[r], seed, t)
+        best = keys.max()
+        kg = int(oracle.block_of_row(ids[r]))
+        assert keys[kg] >= best - KEY_TOL, (r, keys[kg], best)
+        srt = np.sort(keys)
+        if srt[-1] - srt[-2] > KEY_TOL:
+            n_clear += 1
+            assert kg == int(np.argmax(keys)), r
+        row, cum, u = oracle.block_pick(z[r], seed, t, kg)
+        if ids[r] != row:
+            slots = oracle.block_slot_rows(kg, V)
+            q = int(np.flatnonzero(slots == ids[r])[0])
+            lo = 0.0 if q == 0 else np.nanmax(np.concatenate([[0.0], cum[:q]]))
+            assert lo - CUM_TOL <= u <= cum[q] + CUM_TOL, (r, lo, u, cum[q])
+    return n_clear
 
 
 @pytest.mark.parametrize("scaling", [oracle.PER_ROW, oracle.PER_TENSOR, oracle.MX32])
-@pytest.mark.parametrize("T,V,d,inv_temp", [(300, 1000, 256, 1.0), (65, 300, 128, 1 / 0.7)])
+@pytest.mark.parametrize("T,V,d,inv_temp", [(300, 1000, 256, 1.0), (65, 300, 128, 1 / 0.7), (40, 2048, 128, 1.0)])
 def test_sample_matches_oracle(scaling, T, V, d, inv_temp):
     torch, dev = torch_dev()
     from paper_2607_24062_amd import acrl
@@ -48,14 +69,10 @@ def test_sample_matches_oracle(scaling, T, V, d, inv_temp):
     assert np.array_equal(down(hq), hq_o) and np.array_equal(down(wq), wq_o)
     z = np.stack([oracle.logits_mu(hq_o[r], oracle._row_scale(hs_o, scaling, r), wq_o, ws_o, scaling, inv_temp)
                   for r in range(T)])
-    keys = _oracle_keys(z, seed, off)
-    best = keys.max(axis=1)
-    srt = np.sort(keys, axis=1)
-    clear = srt[:, -1] - srt[:, -2] > KEY_TOL
-    want = keys.argmax(axis=1)
-    assert (keys[np.arange(T), ids] >= best - KEY_TOL).all()
-    assert np.array_equal(ids[clear], want[clear])
-    assert clear.mean() > 0.9
+    n_clear = _check_draw(z, ids, seed, off)
+    assert n_clear > 0.9 * T
+    want, _, _ = oracle.block_gumbel_sample(z, seed, off)
+    assert (ids == want).mean() > 0.95
     # log mu of the drawn row
     lse = np.log(np.exp(z - z.max(axis=1, keepdims=True)).sum(axis=1)) + z.max(axis=1)
     np.testing.assert_allclose(lp, z[np.arange(T), ids] - lse, atol=TOL_LOGP, rtol=0)
@@ -88,4 +105,6 @@ def test_sample_chunked_equals_one_shot_and_frequencies():
     p /= p.sum()
     freq = np.bincount(a, minlength=V) / T
     sigma = np.sqrt(p * (1 - p) / T)
-    assert (np.abs(freq - p) < 5 * sigma + 1e-9).all()
+    # 5 standard deviations, plus two draws of slack for rows whose expected
+    # count is far below one (a single draw of such a row is not a bias)
+    assert (np.abs(freq - p) < 5 * sigma + 2.0 / T).all()
