@@ -384,9 +384,10 @@ def library_leg(torch, w, T, H, W, hq, hs, wq, ws, pi_ms, mu_ms, reps=2):
 
 def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, packed, score_ms, reps=2):
     """The scoring call with the full-vocabulary measures (KL both ways,
-    Euclidean distance) switched on: both score kernels also store their
-    logits (4 B each) for passes of 16384 rows and a streaming kernel reads
-    them back (8 B per vocabulary entry and row)."""
+    Euclidean distance) switched on: in passes of 16384 rows the mu kernel
+    also stores its logits (4 B each) and the pi kernel reads them back and
+    accumulates the measures in its epilogue (8 B per vocabulary entry and
+    row in all)."""
     V = w.V
     outs = {}
 
@@ -411,7 +412,7 @@ def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, packed, 
     res = {"what": "acrl_score_pi_mu with kl_pi_mu, kl_mu_pi and l2 over the batch's valid tokens",
            "ms": round(ms, 3), "score_ms_without": round(float(score_ms), 3),
            "overhead_ms": round(ms - float(score_ms), 3),
-           "logit_bytes_stored_and_read": 2 * 4 * T * V * 2,
+           "logit_bytes_stored_and_read": 2 * 4 * T * V,
            "mean_kl_pi_mu": float(kl.double().mean().item()),
            "mean_kl_mu_pi": float(outs["kl_mu_pi"][valid].double().mean().item()),
            "mean_l2": float(outs["l2"][valid].double().mean().item())}

@@ -36,7 +36,9 @@ struct ScorePlan {
   size_t ws_mx_offset[2];    // MX: packed E8M0 scale images of Wq and Hq
   size_t ws_best_offset;     // sampling: the strips' best key, logit and row
   int div_tiles;             // full-vocabulary measures: token tiles per pass (0 = not planned)
-  size_t ws_zbuf_offset[2];  //   the logits of pi and mu of one pass
+  size_t ws_zbuf_offset;     //   mu's logits of one pass
+  size_t ws_aq_offset;       //   mu's lse of the pass rows
+  size_t ws_dpart_offset;    //   pi's strip sums of the measures
   size_t ws_bytes;
 };
 // div_rows > 0 plans the full-vocabulary measures in passes of div_rows rows;

@@ -48,7 +48,8 @@ enum Epilogue {
   kEpiSample = 1,   // the same plus a Gumbel-max draw (sampling from mu)
   kEpiGrad = 2,     // dZ = coef (onehot - softmax) / tau as bf16 operand images (backward)
   kEpiStore = 3,    // the product tile itself, fp32, stored (optionally on top of C)
-  kEpiSoftmaxZ = 4, // kEpiSoftmax + the tile's logits stored (full-vocabulary measures)
+  kEpiSoftmaxZ = 4, // kEpiSoftmax + the tile's logits stored (mu's pass of the full-vocabulary measures)
+  kEpiSoftmaxDiv = 5, // kEpiSoftmax + the measures' sums against mu's stored logits (pi's pass)
 };
 
 constexpr int kTileV = 256;            // vocabulary rows per workgroup tile
@@ -107,11 +108,27 @@ struct ScoreParams {
   int64_t ldc;
   int c_rows;              // valid A rows (M)
   int c_accumulate;        // 1: C += product (C is read once before the K loop)
-  // row chunks and the full-vocabulary measures (kEpiSoftmaxZ)
+  // row chunks and the full-vocabulary measures (kEpiSoftmaxZ, kEpiSoftmaxDiv)
   int tt_offset;           // token tile of this launch's tile 0 (n_ttiles counts the launch's tiles)
-  float* zbuf;             // logits of the launch's rows, row-major [256 n_ttiles][z_ld] (natural units)
-  int64_t z_ld;
+  float* zbuf;             // mu's logits of the launch's rows (natural units), accumulator layout (zbuf_index)
+  const float* aq2;        // [256 n_ttiles] mu's log-sum-exp of the launch's rows, log2 units
+  float* dpart;            // [5][2 n_vtiles][dp_rows] sums of the measures per 128 vocabulary rows (kEpiSoftmaxDiv)
+  int64_t dp_rows;         // row stride of dpart's planes
 };
+
+// Offset (in floats) of the first of the logits lane `lane` holds for 32 x 32
+// block (bv, bt) -- vocabulary rows 32 bv + 8 (i/4) + 4 (lane/32) + i%4,
+// token 32 bt + lane%32 of the tile -- of token tile tt and vocabulary tile
+// vt in the stored logits of a pass.  Each (tt, vt) tile is 256 KiB, each
+// 32 x 32 block 4 KiB; values i = 4m .. 4m + 3 of lane l sit at floats
+// 256 m + 4 l .. 256 m + 4 l + 3 of the block, so one 16-byte access per
+// lane and m moves 1 KiB of contiguous memory per wavefront.  The layout is
+// that of the 32x32 MFMA accumulators, whatever the wave count of the mu
+// kernel that stores and the pi kernel that reads.
+constexpr int kZRun = 256;  // floats between the runs m and m + 1 of a block
+__device__ __forceinline__ int64_t zbuf_index(int tt, int n_vtiles, int vt, int bv, int bt, int lane) {
+  return (((int64_t)tt * n_vtiles + vt) * 64 + bv * 8 + bt) * 1024 + lane * 4;
+}
 
 // Philox4x32-10 (Salmon et al., SC 2011): 10 rounds on a 128-bit counter
 // under a 64-bit key; each round multiplies words 0 and 2 by the round
@@ -271,8 +288,10 @@ void score_kernel(ScoreParams p) {
   constexpr int JT = 16 / NW;   // token blocks of 32 per wave
   constexpr int TW = 32 * JT;   // tokens per wave
   constexpr bool SAMPLE = EPI == kEpiSample;
-  constexpr bool SOFTMAX = EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ;
+  constexpr bool DIV = EPI == kEpiSoftmaxDiv;
+  constexpr bool SOFTMAX = EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ || DIV;
   static_assert(MODE == kBF16 || SOFTMAX, "the backward epilogues take bf16 operands");
+  static_assert(!DIV || MODE == kBF16, "the measures are accumulated in pi's pass");
   constexpr int NS = Pipe<MODE>::kStages;
   // FP8 per-tensor / MX scorers start each tile's accumulators with an
   // inline-zero MFMA instead of clearing them after the epilogue (measured:
@@ -511,6 +530,22 @@ void score_kernel(ScoreParams p) {
     // keep the tail weights derived from nv inside the epilogue (else they
     // are computed before the K loop and held across it)
     asm volatile("v_mov_b32 %0, %0" : "+v"(nv));
+    // full-vocabulary measures: mu's lse (log2 units) of the lane's tokens
+    // and the tile's five sums per token (live only in the epilogue)
+    float a2[4], dv[5][4];
+    // the lane's token row in the tile and its 128-row slot of the sums,
+    // formed here through an opaque move (else the addresses below are
+    // hoisted out of the tile loop and held across it)
+    int dv_row = wt * TW + r32, dv_slot = wv;
+    asm volatile("v_mov_b32 %0, %0\n\tv_mov_b32 %1, %1" : "+v"(dv_row), "+v"(dv_slot));
+    if constexpr (DIV) {
+#pragma unroll
+      for (int j = 0; j < JT; ++j) {
+        a2[j] = p.aq2[tt * kTileT + dv_row + j * 32];
+#pragma unroll
+        for (int c = 0; c < 5; ++c) dv[c][j] = 0.0f;
+      }
+    }
     // The pass, written for instruction-level parallelism (one wave per
     // SIMD: nothing else hides latencies): all 16 exponents of a block are
     // formed before any is used, maxima and sums are trees.  The tail tile
@@ -541,12 +576,16 @@ void score_kernel(ScoreParams p) {
             if constexpr (MODE == kFP8Row) v[i] *= rs[i];
           }
           if constexpr (EPI == kEpiSoftmaxZ) {
-            // the logits z = acc * scale (natural units) of the lane's token
-            // row: 4 runs of 4 consecutive vocabulary entries (16 bytes each)
-            float* zr = p.zbuf + (int64_t)(tt * kTileT + wt * TW + j * 32 + r32) * p.z_ld + v0 + 32 * b + 4 * g;
+            // the logits z = acc * scale (natural units) of the block, as the
+            // lane holds them (64 contiguous bytes)
+            // (the lane's offset passes through an opaque move, else the
+            // offsets of all blocks are formed once and held across the loop)
+            int zo = (int)zbuf_index(0, 0, 0, wv * 4 + b, wt * JT + j, lane);
+            asm volatile("v_mov_b32 %0, %0" : "+v"(zo));
+            float* zr = p.zbuf + zbuf_index(tt, p.n_vtiles, tile, 0, 0, 0) + zo;
 #pragma unroll
             for (int qq = 0; qq < 4; ++qq)
-              *reinterpret_cast<f32x4*>(zr + 8 * qq) =
+              *reinterpret_cast<f32x4*>(zr + kZRun * qq) =
                   f32x4{v[4 * qq] * cz[j], v[4 * qq + 1] * cz[j], v[4 * qq + 2] * cz[j], v[4 * qq + 3] * cz[j]};
           }
           float mx[8];
@@ -678,13 +717,90 @@ void score_kernel(ScoreParams p) {
             for (int i = 0; i < 16; ++i) z = fmaf(fmaxf(1.0f - fabsf(fi - (float)i), 0.0f), v[i], z);
             if (tok[j] < p.n_rows && id[j] < p.V) p.logit[tok[j]] = z * cz[j];
           }
+          if constexpr (DIV) {
+            // no contraction in this block: z = acc * c must be rounded as
+            // mu's pass rounds the logits it stores (an fma of z - zq would
+            // leave the product's rounding error where equal logits need 0)
+#pragma clang fp contract(off)
+            // Full-vocabulary measures against mu's logits zq and mu's final
+            // lse A_q: with pt = exp(z - A_q) and q = exp(zq - A_q) (so that
+            // p = pt exp(A_q - A_p)), the sums of pt (z - zq), q (zq - z),
+            // (pt - q)^2, (pt - q) pt and pt^2 over the vocabulary give both
+            // KL divergences and |p - q|_2 exactly once A_p is known
+            // (div_finalize_kernel).  No running maximum enters, so the sums
+            // need no rescaling; pt and q come from one formula, so equal
+            // logits give pt == q bit for bit.  The logits are read out of
+            // the accumulators again, four at a time (fewer live registers
+            // than keeping the 16 of the softmax pass).  mu's logits of the
+            // same 16 entries were stored by mu's pass.
+            // (the lane offset passes through an opaque move here, so that the
+            // loads are issued at this point and not hoisted ahead of the
+            // softmax pass, where their registers would be spilled)
+            int zo = (int)zbuf_index(0, 0, 0, wv * 4 + b, wt * JT + j, lane);
+            asm volatile("v_mov_b32 %0, %0" : "+v"(zo));
+            const float* zr = p.zbuf + zbuf_index(tt, p.n_vtiles, tile, 0, 0, 0) + zo;
+            float zq[16];
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+              const f32x4 f = *reinterpret_cast<const f32x4*>(zr + kZRun * qq);
+              zq[4 * qq] = f[0]; zq[4 * qq + 1] = f[1]; zq[4 * qq + 2] = f[2]; zq[4 * qq + 3] = f[3];
+            }
+            float k1 = 0.0f, k2 = 0.0f, la = 0.0f, lb = 0.0f, lc = 0.0f;
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+#pragma unroll
+              for (int ii = 0; ii < 4; ++ii) {
+                const int i = 4 * qq + ii;
+                const float zp = acc_read(acc[b][j][i]) * cz[j];
+                float ep = fast_exp2(fmaf(zp, kLog2e, -a2[j]));
+                float eq = fast_exp2(fmaf(zq[i], kLog2e, -a2[j]));
+                if constexpr (kTail) {
+                  const float wt1 = fminf(fmaxf(nv - (float)(16 * b + i), 0.0f), 1.0f);
+                  ep *= wt1;
+                  eq *= wt1;
+                }
+                const float dz = zp - zq[i], dd = ep - eq;
+                k1 = fmaf(ep, dz, k1);
+                k2 = fmaf(-eq, dz, k2);
+                la = fmaf(dd, dd, la);
+                lb = fmaf(dd, ep, lb);
+                lc = fmaf(ep, ep, lc);
+              }
+              __builtin_amdgcn_sched_barrier(0);
+            }
+            dv[0][j] += k1;
+            dv[1][j] += k2;
+            dv[2][j] += la;
+            dv[3][j] += lb;
+            dv[4][j] += lc;
+            // complete the sums here (else they are sunk to their use at the
+            // end of the tile and the loaded values of every block stay live)
+            asm volatile("" : "+v"(dv[0][j]), "+v"(dv[1][j]), "+v"(dv[2][j]), "+v"(dv[3][j]), "+v"(dv[4][j]));
+          }
           __builtin_amdgcn_sched_barrier(0);
         }
       }
     };
     if (partial) run(std::true_type{});
     else run(std::false_type{});
-    if constexpr (EPI == kEpiSoftmaxZ) wait_vmcnt<0>();  // stores must not count in the pipeline's waits
+    if constexpr (DIV) {
+      // the tile's sums per token: lanes l and l ^ 32 (the two 4-row halves
+      // of every 8 rows) add up, then one lane stores the wave's 128-row
+      // share, slot 2 tile + wv of the pass row
+      const int64_t plane = (int64_t)p.n_vtiles * 2 * p.dp_rows;
+#pragma unroll
+      for (int j = 0; j < JT; ++j) {
+#pragma unroll
+        for (int c = 0; c < 5; ++c) dv[c][j] += __shfl_xor(dv[c][j], 32);
+        if (g == 0) {
+          const int64_t o = (int64_t)(2 * tile + dv_slot) * p.dp_rows + tt * kTileT + dv_row + j * 32;
+#pragma unroll
+          for (int c = 0; c < 5; ++c) p.dpart[c * plane + o] = dv[c][j];
+        }
+      }
+    }
+    // stores must not count in the pipeline's waits
+    if constexpr (EPI == kEpiSoftmaxZ || DIV) wait_vmcnt<0>();
   };
 
   // Backward (kEpiGrad): dZ[t, v] = coef_t (delta(v, a_t) - p_tv) / tau of the
@@ -964,7 +1080,6 @@ void score_kernel(ScoreParams p) {
           p.best_logit[o] = bz[j];
           p.best_id[o] = bi[j];
         }
-
       }
     }
   }
@@ -978,7 +1093,8 @@ void score_kernel(ScoreParams p) {
 // 85.4 ms, q17b 27.0 vs 30.6 ms), where they spill around the epilogue.
 template <int MODE, int EPI>
 constexpr int waves_for() {
-  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) || (EPI == kEpiSoftmaxZ && MODE == kBF16))
+  return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) ||
+          (EPI == kEpiSoftmaxZ && (MODE == kFP8Tensor || MODE == kFP8Row)) || (EPI == kEpiSoftmaxDiv && MODE == kBF16))
              ? 8
              : 4;
 }
@@ -1094,14 +1210,26 @@ __device__ __forceinline__ float merged_lse2(const float* part, int64_t plane, i
   return M + log2f(S);
 }
 
+// mu's log-sum-exp (log2 units) of rows r0 .. r0 + rows - 1 for the pi pass
+// of the full-vocabulary measures; entries rows .. cap - 1 (token-tile
+// padding) get 0.
+__global__ __launch_bounds__(256) void lse2_kernel(const float* __restrict__ part, int n_strips, int n_rows, int r0,
+                                                   int rows, int cap, float* __restrict__ out) {
+  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= cap) return;
+  out[k] = k < rows ? merged_lse2(part, (int64_t)n_strips * n_rows, n_strips, n_rows, r0 + k) : 0.0f;
+}
+
 struct DivParams {
   int n_rows;              // rows of the whole call
   int n_strips;
-  int V;
-  int r0;                  // first row of this pass (row r0 + k is row k of the stored logits)
-  int64_t z_ld;
-  const float* z[2];       // logits of the pass's rows, pi and mu
-  const float* part[2];    // the strips' (M, S, U) states of pi and mu
+  int r0;                  // first row of this pass
+  int rows;                // rows of this pass
+  int n_parts;             // partial sums per row: 2 per vocabulary tile
+  int64_t dp_rows;         // row stride of dpart's planes
+  const float* part_pi;    // pi's (M, S, U) strip states
+  const float* aq2;        // mu's lse of the pass rows (log2 units)
+  const float* dpart;      // [5][n_parts][dp_rows] sums per 128 vocabulary rows
   const uint8_t* mask;
   const int32_t* out_slot;
   float* kl_pm;            // [slots] KL(pi || mu), nullable
@@ -1109,59 +1237,59 @@ struct DivParams {
   float* l2;               // [slots] Euclidean distance, nullable
 };
 
-// Full-vocabulary measures of one row per workgroup, from the stored logits
-// of both policies and their log-sum-exps A (log2 units): p = 2^(z_pi log2e
-// - A_pi), q likewise, and the log-ratio l_p - l_q formed as
-// (z_pi - z_mu) - (A_pi - A_mu) ln 2 so that its terms are small (and exactly
-// 0 for identical policies, whatever the compiler fuses):
-// KL(pi||mu) = sum p (l_p - l_q), KL(mu||pi) = sum q (l_q - l_p),
-// |p - q|_2 = sqrt(sum (p - q)^2).  fp32 sums per thread, then a fixed tree.
-__global__ __launch_bounds__(256) void divergence_kernel(DivParams p) {
-  const int k = blockIdx.x;
-  const int r = p.r0 + k;
-  const int64_t plane = (int64_t)p.n_strips * p.n_rows;
-  const bool active = p.mask ? p.mask[r] != 0 : true;
-  float a = 0.f, b = 0.f, c = 0.f;
+// The measures of the pass rows from the pi kernel's sums (one per 128
+// vocabulary rows), taken against mu's lse A_q.  A workgroup takes 32 rows;
+// its 8 thread groups add the parts s = g, g + 8, ... of each row, and one
+// thread per row adds the 8 group sums in order.  With D = A_p - A_q (nats)
+// and r = exp(-D), so that p = r pt:
+//   KL(pi||mu) = sum p ((z - zq) - D) = r sum pt (z - zq) - D,
+//   KL(mu||pi) = sum q ((zq - z) + D) = sum q (zq - z) + D,
+//   |p - q|^2  = sum ((pt - q) + (r - 1) pt)^2
+//              = sum (pt - q)^2 + 2 (r - 1) sum (pt - q) pt + (r - 1)^2 sum pt^2,
+// using sum p = sum q = 1.  Every term is small for nearby policies, so no
+// large quantities cancel.  pt = exp(z - A_q) is formed in fp32: rows with
+// |D| > 64 (where it could overflow) get NaN.
+constexpr int kFinRows = 32, kFinGroups = 8;
+__global__ __launch_bounds__(kFinRows * kFinGroups) void div_finalize_kernel(DivParams p) {
+  __shared__ float part_sums[5][kFinGroups][kFinRows];
+  const int rl = threadIdx.x % kFinRows, grp = threadIdx.x / kFinRows;
+  const int k = blockIdx.x * kFinRows + rl;
+  const bool in = k < p.rows;
+  const int r = p.r0 + (in ? k : 0);
+  const bool active = in && (p.mask ? p.mask[r] != 0 : true);
+  float sum[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
   if (active) {
-    const float ap = merged_lse2(p.part[0], plane, p.n_strips, p.n_rows, r);
-    const float aq = merged_lse2(p.part[1], plane, p.n_strips, p.n_rows, r);
-    const float dl = (ap - aq) * kLn2;
-    const float* zp = p.z[0] + (int64_t)k * p.z_ld;
-    const float* zq = p.z[1] + (int64_t)k * p.z_ld;
-    for (int v = threadIdx.x * 4; v < p.V; v += 1024) {
-      const f32x4 x = *reinterpret_cast<const f32x4*>(zp + v);
-      const f32x4 y = *reinterpret_cast<const f32x4*>(zq + v);
+    const int64_t plane = (int64_t)p.n_parts * p.dp_rows;
+    for (int s = grp; s < p.n_parts; s += kFinGroups)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        if (v + i < p.V) {
-          const float pr = fast_exp2(fmaf(x[i], kLog2e, -ap));
-          const float qr = fast_exp2(fmaf(y[i], kLog2e, -aq));
-          const float lr = (x[i] - y[i]) - dl;  // l_p - l_q
-          a = fmaf(pr, lr, a);
-          b = fmaf(-qr, lr, b);
-          c = fmaf(pr - qr, pr - qr, c);
-        }
-      }
-    }
+      for (int c = 0; c < 5; ++c) sum[c] += p.dpart[c * plane + (int64_t)s * p.dp_rows + k];
   }
-  __shared__ float sh[3][256];
-  sh[0][threadIdx.x] = a;
-  sh[1][threadIdx.x] = b;
-  sh[2][threadIdx.x] = c;
+#pragma unroll
+  for (int c = 0; c < 5; ++c) part_sums[c][grp][rl] = sum[c];
   __syncthreads();
-  for (int w = 128; w >= 1; w >>= 1) {
-    if ((int)threadIdx.x < w) {
+  if (grp != 0 || !in) return;
+  float kpm = 0.f, kmp = 0.f, l2 = 0.f;
+  if (active) {
 #pragma unroll
-      for (int q = 0; q < 3; ++q) sh[q][threadIdx.x] += sh[q][threadIdx.x + w];
+    for (int c = 0; c < 5; ++c) {
+      sum[c] = part_sums[c][0][rl];
+      for (int g2 = 1; g2 < kFinGroups; ++g2) sum[c] += part_sums[c][g2][rl];
     }
-    __syncthreads();
+    const float ap = merged_lse2(p.part_pi, (int64_t)p.n_strips * p.n_rows, p.n_strips, p.n_rows, r);
+    const float D = (ap - p.aq2[k]) * kLn2;
+    if (fabsf(D) <= 64.0f) {
+      const float rm1 = expm1f(-D);
+      kpm = fmaf(rm1, sum[0], sum[0]) - D;
+      kmp = sum[1] + D;
+      l2 = sqrtf(fmaxf(sum[2] + rm1 * (2.0f * sum[3] + rm1 * sum[4]), 0.0f));
+    } else {
+      kpm = kmp = l2 = __builtin_nanf("");
+    }
   }
-  if (threadIdx.x == 0) {
-    const int slot = p.out_slot ? p.out_slot[r] : r;
-    if (p.kl_pm) p.kl_pm[slot] = sh[0][0];
-    if (p.kl_mp) p.kl_mp[slot] = sh[1][0];
-    if (p.l2) p.l2[slot] = sqrtf(sh[2][0]);
-  }
+  const int slot = p.out_slot ? p.out_slot[r] : r;
+  if (p.kl_pm) p.kl_pm[slot] = kpm;
+  if (p.kl_mp) p.kl_mp[slot] = kmp;
+  if (p.l2) p.l2[slot] = l2;
 }
 
 struct MergeParams {
@@ -1349,18 +1477,21 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows, boo
     pl.ws_mx_offset[q] = off;
     if (!(prepacked && q == 0)) off += align_up(mx_bytes[q], 256);
   }
-  // full-vocabulary measures: the logits of both policies for one pass of
-  // div_tiles token tiles, row-major with the padded vocabulary as stride
+  // full-vocabulary measures, per pass of div_tiles token tiles: mu's
+  // logits (256 KiB per pair of token and vocabulary tiles), mu's lse of the
+  // pass rows and pi's five sums per row and 128 vocabulary rows
   pl.div_tiles = 0;
   if (div_rows > 0) {
     const int64_t rows = std::min<int64_t>((div_rows + kTileT - 1) / kTileT * kTileT,
                                            (int64_t)pl.n_ttiles * kTileT);
     pl.div_tiles = (int)std::max<int64_t>(rows / kTileT, 1);
-    const size_t zb = (size_t)pl.div_tiles * kTileT * pl.n_vtiles * kTileV * sizeof(float);
-    pl.ws_zbuf_offset[0] = off;
-    off += zb;
-    pl.ws_zbuf_offset[1] = off;
-    off += zb;
+    const size_t prow = (size_t)pl.div_tiles * kTileT;
+    pl.ws_zbuf_offset = off;
+    off += prow * pl.n_vtiles * kTileV * sizeof(float);
+    pl.ws_aq_offset = off;
+    off += align_up(prow * sizeof(float), 256);
+    pl.ws_dpart_offset = off;
+    off += align_up((size_t)5 * 2 * pl.n_vtiles * prow * sizeof(float), 256);
   }
   pl.ws_bytes = off;
   return pl;
@@ -1440,46 +1571,53 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
     if (do_pi) launch_score_kernel<kBF16, kEpiSoftmax>(grid, pp, s);
     if (do_mu) launch_mu(pm, grid, std::integral_constant<int, kEpiSoftmax>{});
   } else {
-    // passes of div_tiles token tiles: pi and mu (softmax + the logits
-    // stored), then the measures of the pass's rows
-    float* zbuf[2] = {reinterpret_cast<float*>(ws + pl.ws_zbuf_offset[0]),
-                      reinterpret_cast<float*>(ws + pl.ws_zbuf_offset[1])};
-    const int64_t z_ld = (int64_t)pl.n_vtiles * kTileV;
+    // passes of div_tiles token tiles: mu (softmax + its logits stored),
+    // mu's lse of the pass rows, pi (softmax + the measures' sums against
+    // mu's logits), then the measures of the pass rows
+    float* zq = reinterpret_cast<float*>(ws + pl.ws_zbuf_offset);
+    float* aq2 = reinterpret_cast<float*>(ws + pl.ws_aq_offset);
+    float* dpart = reinterpret_cast<float*>(ws + pl.ws_dpart_offset);
+    const int cap = pl.div_tiles * kTileT;
     for (int tt0 = 0; tt0 < pl.n_ttiles; tt0 += pl.div_tiles) {
       const int nt = std::min(pl.div_tiles, pl.n_ttiles - tt0);
       const int ntb = (nt + kBlockT - 1) / kBlockT;
       const unsigned g = (unsigned)((ntb * pl.n_sblocks + kXcds - 1) / kXcds * kXcds * kBlockT * kBlockS);
-      ScoreParams pz = pp;
-      pz.tt_offset = tt0;
-      pz.n_ttiles = nt;
-      pz.n_tblocks = ntb;
-      pz.zbuf = zbuf[0];
-      pz.z_ld = z_ld;
-      launch_score_kernel<kBF16, kEpiSoftmaxZ>(g, pz, s);
+      const int r0 = tt0 * kTileT;
+      const int rows = (int)std::min<int64_t>(dsc.n_rows - r0, (int64_t)nt * kTileT);
       ScoreParams pq = pm;
       pq.tt_offset = tt0;
       pq.n_ttiles = nt;
       pq.n_tblocks = ntb;
-      pq.zbuf = zbuf[1];
-      pq.z_ld = z_ld;
+      pq.zbuf = zq;
       launch_mu(pq, g, std::integral_constant<int, kEpiSoftmaxZ>{});
+      hipLaunchKernelGGL(lse2_kernel, dim3((unsigned)((cap + 255) / 256)), dim3(256), 0, s, pm.part, pl.n_strips,
+                         (int)dsc.n_rows, r0, rows, cap, aq2);
+      ScoreParams pz = pp;
+      pz.tt_offset = tt0;
+      pz.n_ttiles = nt;
+      pz.n_tblocks = ntb;
+      pz.zbuf = zq;
+      pz.aq2 = aq2;
+      pz.dpart = dpart;
+      pz.dp_rows = cap;
+      launch_score_kernel<kBF16, kEpiSoftmaxDiv>(g, pz, s);
       DivParams dp{};
       dp.n_rows = (int)dsc.n_rows;
       dp.n_strips = pl.n_strips;
-      dp.V = (int)dsc.V;
-      dp.r0 = tt0 * kTileT;
-      dp.z_ld = z_ld;
-      dp.z[0] = zbuf[0];
-      dp.z[1] = zbuf[1];
-      dp.part[0] = pp.part;
-      dp.part[1] = pm.part;
+      dp.r0 = r0;
+      dp.rows = rows;
+      dp.n_parts = 2 * pl.n_vtiles;
+      dp.dp_rows = cap;
+      dp.part_pi = pp.part;
+      dp.aq2 = aq2;
+      dp.dpart = dpart;
       dp.mask = dsc.mask;
       dp.out_slot = dsc.out_slot;
       dp.kl_pm = dsc.kl_pi_mu;
       dp.kl_mp = dsc.kl_mu_pi;
       dp.l2 = dsc.l2;
-      const int rows = (int)std::min<int64_t>(dsc.n_rows - dp.r0, (int64_t)nt * kTileT);
-      hipLaunchKernelGGL(divergence_kernel, dim3((unsigned)rows), dim3(256), 0, s, dp);
+      hipLaunchKernelGGL(div_finalize_kernel, dim3((unsigned)((rows + kFinRows - 1) / kFinRows)),
+                         dim3(kFinRows * kFinGroups), 0, s, dp);
     }
   }
 
