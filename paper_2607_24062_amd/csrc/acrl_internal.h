@@ -39,6 +39,7 @@ struct ScorePlan {
   size_t ws_zbuf_offset;     //   mu's logits of one pass
   size_t ws_aq_offset;       //   mu's lse of the pass rows
   size_t ws_dpart_offset;    //   pi's strip sums of the measures
+  size_t ws_queue_offset;    // the persistent grid's per-XCD claim counters
   size_t ws_bytes;
 };
 // div_rows > 0 plans the full-vocabulary measures in passes of div_rows rows;

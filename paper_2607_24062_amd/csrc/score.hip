@@ -114,7 +114,12 @@ struct ScoreParams {
   const float* aq2;        // [256 n_ttiles] mu's log-sum-exp of the launch's rows, log2 units
   float* dpart;            // [5][2 n_vtiles][dp_rows] sums of the measures per 128 vocabulary rows (kEpiSoftmaxDiv)
   int64_t dp_rows;         // row stride of dpart's planes
+  // persistent grid: one claim counter per XCD (kQueueStride ints apart,
+  // zero at launch) and the units in each XCD's queue
+  int* queue;
+  int units_per_xcd;
 };
+constexpr int kQueueStride = 16;  // 64 bytes between the XCDs' counters
 
 // Offset (in floats) of the first of the logits lane `lane` holds for 32 x 32
 // block (bv, bt) -- vocabulary rows 32 bv + 8 (i/4) + 4 (lane/32) + i%4,
@@ -159,6 +164,7 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // Combine two partial softmax states (log2 units).
 __device__ __forceinline__ void merge_state(float& M, float& S, float& U, float M2, float S2,
                                             float U2) {
+#pragma clang fp contract(off)
   if (S2 == 0.0f) return;  // empty state (its M is only a reference point)
   if (S == 0.0f) {
     M = M2; S = S2; U = U2;
@@ -281,7 +287,9 @@ struct Pipe {
 // per SIMD, each 128 x 64 (4 x 2 blocks, 128 accumulators): while one wave
 // waits at the chunk barrier or runs its softmax epilogue the other keeps
 // the SIMD's matrix core busy.
-template <int MODE, int EPI, int NW>
+// PERSIST: one workgroup per CU claims units from per-XCD queues (below);
+// otherwise one workgroup per unit.
+template <int MODE, int EPI, int NW, bool PERSIST>
 __global__ __attribute__((amdgpu_flat_work_group_size(NW * 64, NW * 64), amdgpu_waves_per_eu(NW / 4, NW / 4)))
 void score_kernel(ScoreParams p) {
   static_assert(NW == 4 || NW == 8, "4 or 8 waves");
@@ -309,16 +317,9 @@ void score_kernel(ScoreParams p) {
   const int r32 = lane & 31, g = lane >> 5;
   const int sw = (lane >> 2) & 3;  // swizzle of this lane's fragment row (see below)
 
-  // ---- which (token tile, strip) this workgroup owns
-  int tt, st;
-  {
-    const int xcd = blockIdx.x % kXcds, i = blockIdx.x / kXcds;
-    const int per = kBlockT * kBlockS;
-    const int blk = (i / per) * kXcds + xcd;  // blocks in dispatch order, 8 at a time
-    const int k = i % per;
-    tt = (blk % p.n_tblocks) * kBlockT + k / kBlockS;
-    st = (blk / p.n_tblocks) * kBlockS + k % kBlockS;
-  }
+  // ---- one unit of work: token tile tt (of the launch) against vocabulary
+  // strip st (the dispatch below picks the units)
+  auto unit = [&](int tt, int st) {
   if (tt >= p.n_ttiles || st >= p.n_strips) return;  // padding of the grid
   const int ttg = tt + p.tt_offset;  // token tile in the whole call
   const int t0 = ttg * kTileT;
@@ -551,6 +552,9 @@ void score_kernel(ScoreParams p) {
     // formed before any is used, maxima and sums are trees.  The tail tile
     // (rows past V present) takes its own copy of the code.
     auto run = [&](auto tail_tag) {
+      // every fused multiply-add below is written out (fmaf): no contraction
+      // of the rest, so every variant rounds the statistics alike
+#pragma clang fp contract(off)
       constexpr bool kTail = decltype(tail_tag)::value;
       uint32_t pw[JT][2];  // sampling: the Philox words the odd block of a pair uses
       (void)pw;
@@ -1083,7 +1087,50 @@ void score_kernel(ScoreParams p) {
       }
     }
   }
+  };  // unit
+
+  // ---- which units this workgroup runs.  Unit i of XCD x is the i-th
+  // workgroup that XCD would get from a grid of one workgroup per unit
+  // (workgroups go to the XCDs round robin): blocks of kBlockT token tiles x
+  // kBlockS strips, so that an XCD's concurrent units share W and H chunks
+  // in its L2.  Persistent: one workgroup per CU takes the next unit of its
+  // own XCD's queue, and once that is empty the next of the other XCDs'
+  // queues, so that XCDs that run faster take more units (a fixed share per
+  // XCD leaves the faster ones idle at the end).  Every claim is one atomic
+  // on the queue's counter; a workgroup exits once every queue is empty.
+  constexpr int per = kBlockT * kBlockS;
+  auto run_unit = [&](int x, int i) {
+    const int blk = (i / per) * kXcds + x, k = i % per;
+    unit((blk % p.n_tblocks) * kBlockT + k / kBlockS, (blk / p.n_tblocks) * kBlockS + k % kBlockS);
+  };
+  if constexpr (!PERSIST) {
+    run_unit((int)(blockIdx.x % kXcds), (int)(blockIdx.x / kXcds));
+  } else {
+    // the XCD this workgroup runs on (XCC_ID hardware register, bits 3:0)
+    const int xcc = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & (kXcds - 1));
+    int* slot = reinterpret_cast<int*>(lds);  // the stages are free between units
+    for (;;) {
+      if (tid == 0) {
+        int claim = -1;
+        for (int a = 0; a < kXcds && claim < 0; ++a) {
+          const int x = (xcc + a) & (kXcds - 1);
+          const int t = atomicAdd(p.queue + kQueueStride * x, 1);
+          if (t < p.units_per_xcd) claim = x * p.units_per_xcd + t;
+        }
+        *slot = claim;
+      }
+      __syncthreads();
+      const int c = *slot;
+      __syncthreads();  // every wave has its claim before the stages are written
+      if (c < 0) break;
+      const int x = c / p.units_per_xcd;
+      run_unit(x, c - x * p.units_per_xcd);
+      __syncthreads();  // the unit's last LDS reads are done
+    }
+  }
 }
+
+__global__ void clear_queue_kernel(int* q) { q[kQueueStride * threadIdx.x] = 0; }
 
 // Waves per workgroup of each instantiation (measured on the MI355X): two
 // per SIMD where the variant runs faster that way (the per-row FP8 scorer
@@ -1099,10 +1146,36 @@ constexpr int waves_for() {
              : 4;
 }
 
+// Scoring launches: `grid` units (a multiple of kXcds).  The softmax
+// epilogues run persistent, one workgroup per CU (measured on the MI355X,
+// against one workgroup per unit, results bitwise equal: pi 5 % faster at
+// d = 4096 and 5120, 3 % at d = 2048; per-tensor FP8 mu 2.5 %, MX 1 %),
+// except the 8-wave per-row FP8 kernels, which the unit loop pushes into
+// spills (112 bytes per lane; q17b mu 4 % slower).  p.queue must point at
+// kXcds * kQueueStride ints of workspace, cleared here.  The backward
+// products take one workgroup per unit.
+inline int device_cus() {
+  int dev = 0, n = 0;
+  if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n <= 0)
+    n = 256;
+  return n;
+}
+
 template <int MODE, int EPI>
 void launch_score_kernel(unsigned grid, const ScoreParams& p, hipStream_t s) {
   constexpr int NW = waves_for<MODE, EPI>();
-  hipLaunchKernelGGL((score_kernel<MODE, EPI, NW>), dim3(grid), dim3(NW * 64), 0, s, p);
+  constexpr bool kPersist = (EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ || EPI == kEpiSoftmaxDiv) &&
+                            !(MODE == kFP8Row && NW == 8);
+  if constexpr (kPersist) {
+    ScoreParams q = p;
+    q.units_per_xcd = (int)(grid / kXcds);
+    hipLaunchKernelGGL(clear_queue_kernel, dim3(1), dim3(kXcds), 0, s, q.queue);
+    const unsigned wgs = std::min<unsigned>(grid, (unsigned)device_cus());
+    hipLaunchKernelGGL((score_kernel<MODE, EPI, NW, true>), dim3(wgs), dim3(NW * 64), 0, s, q);
+  } else {
+    hipLaunchKernelGGL((score_kernel<MODE, EPI, NW, false>), dim3(grid), dim3(NW * 64), 0, s, p);
+  }
 }
 
 // Packed operand image read by score_kernel: for each 256-row tile and each
@@ -1493,6 +1566,9 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows, boo
     pl.ws_dpart_offset = off;
     off += align_up((size_t)5 * 2 * pl.n_vtiles * prow * sizeof(float), 256);
   }
+  // the persistent grid's per-XCD claim counters (cleared before each launch)
+  pl.ws_queue_offset = off;
+  off += align_up((size_t)kXcds * kQueueStride * sizeof(int), 256);
   pl.ws_bytes = off;
   return pl;
 }
@@ -1513,6 +1589,7 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
   pp.inv_temp = dsc.inv_temperature;
   pp.ids = dsc.token_ids;
   pp.mx_row_bytes = (int)(dsc.d / 32);
+  pp.queue = reinterpret_cast<int*>(ws + pl.ws_queue_offset);
 
   const bool do_pi = dsc.policies != ACRL_POLICY_MU;
   const bool do_mu = dsc.policies != ACRL_POLICY_PI;
@@ -1810,6 +1887,7 @@ hipError_t launch_sample(const acrl_sample_desc& dsc, const ScorePlan& pl, hipSt
   pm.n_tblocks = pl.n_tblocks;
   pm.inv_temp = dsc.inv_temperature;
   pm.mx_row_bytes = (int)(dsc.d / 32);
+  pm.queue = reinterpret_cast<int*>(ws + pl.ws_queue_offset);
   pm.a = pw ? pw + pwl.wq_offset : ws + pl.ws_pack_offset[2];
   pm.b = ws + pl.ws_pack_offset[3];
   pm.n_chunks = (int)(dsc.d / kChunk);
