@@ -174,7 +174,7 @@ acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, vo
  * kept in the workspace (4 bytes per logit), and the pi kernel that follows
  * reads them back and accumulates the three measures against mu's lse; the
  * workspace must have acrl_score_div_workspace_size() bytes.  The terms are
- * formed in fp32 relative to mu's lse: rows where |lse_pi - lse_mu| > 64
+ * formed in fp32 relative to mu's lse: rows where |lse_pi - lse_mu| > 32
  * get NaN measures (such policies have nothing in common numerically).
  */
 typedef struct acrl_score_desc {

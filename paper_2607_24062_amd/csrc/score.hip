@@ -589,8 +589,9 @@ void score_kernel(ScoreParams p) {
             float* zr = p.zbuf + zbuf_index(tt, p.n_vtiles, tile, 0, 0, 0) + zo;
 #pragma unroll
             for (int qq = 0; qq < 4; ++qq)
-              *reinterpret_cast<f32x4*>(zr + kZRun * qq) =
-                  f32x4{v[4 * qq] * cz[j], v[4 * qq + 1] * cz[j], v[4 * qq + 2] * cz[j], v[4 * qq + 3] * cz[j]};
+              __builtin_nontemporal_store(  // streamed: read back once, by the pi pass
+                  f32x4{v[4 * qq] * cz[j], v[4 * qq + 1] * cz[j], v[4 * qq + 2] * cz[j], v[4 * qq + 3] * cz[j]},
+                  reinterpret_cast<f32x4*>(zr + kZRun * qq));
           }
           float mx[8];
 #pragma unroll
@@ -746,7 +747,7 @@ void score_kernel(ScoreParams p) {
             float zq[16];
 #pragma unroll
             for (int qq = 0; qq < 4; ++qq) {
-              const f32x4 f = *reinterpret_cast<const f32x4*>(zr + kZRun * qq);
+              const f32x4 f = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(zr + kZRun * qq));
               zq[4 * qq] = f[0]; zq[4 * qq + 1] = f[1]; zq[4 * qq + 2] = f[2]; zq[4 * qq + 3] = f[3];
             }
             float k1 = 0.0f, k2 = 0.0f, la = 0.0f, lb = 0.0f, lc = 0.0f;
@@ -1320,8 +1321,8 @@ struct DivParams {
 //   |p - q|^2  = sum ((pt - q) + (r - 1) pt)^2
 //              = sum (pt - q)^2 + 2 (r - 1) sum (pt - q) pt + (r - 1)^2 sum pt^2,
 // using sum p = sum q = 1.  Every term is small for nearby policies, so no
-// large quantities cancel.  pt = exp(z - A_q) is formed in fp32: rows with
-// |D| > 64 (where it could overflow) get NaN.
+// large quantities cancel.  pt = exp(z - A_q) <= exp(D) and pt^2 are formed
+// in fp32: rows with |D| > 32 nats (where they could overflow) get NaN.
 constexpr int kFinRows = 32, kFinGroups = 8;
 __global__ __launch_bounds__(kFinRows * kFinGroups) void div_finalize_kernel(DivParams p) {
   __shared__ float part_sums[5][kFinGroups][kFinRows];
@@ -1350,7 +1351,7 @@ __global__ __launch_bounds__(kFinRows * kFinGroups) void div_finalize_kernel(Div
     }
     const float ap = merged_lse2(p.part_pi, (int64_t)p.n_strips * p.n_rows, p.n_strips, p.n_rows, r);
     const float D = (ap - p.aq2[k]) * kLn2;
-    if (fabsf(D) <= 64.0f) {
+    if (fabsf(D) <= 32.0f) {
       const float rm1 = expm1f(-D);
       kpm = fmaf(rm1, sum[0], sum[0]) - D;
       kmp = sum[1] + D;
