@@ -175,7 +175,10 @@ acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, vo
  * reads them back and accumulates the three measures against mu's lse; the
  * workspace must have acrl_score_div_workspace_size() bytes.  The terms are
  * formed in fp32 relative to mu's lse: rows where |lse_pi - lse_mu| > 32
- * get NaN measures (such policies have nothing in common numerically).
+ * get NaN measures (such policies have nothing in common numerically), and
+ * l2 is NaN where its terms cancel so far that its error could exceed ~1e-4
+ * (lse_pi several nats above lse_mu; policies that differ by quantization
+ * stay far inside).
  */
 typedef struct acrl_score_desc {
   int64_t n_rows;               /* rows scored by this call (a chunk of the batch is fine) */

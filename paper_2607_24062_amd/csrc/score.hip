@@ -1322,21 +1322,27 @@ struct DivParams {
 //              = sum (pt - q)^2 + 2 (r - 1) sum (pt - q) pt + (r - 1)^2 sum pt^2,
 // using sum p = sum q = 1.  Every term is small for nearby policies, so no
 // large quantities cancel.  pt = exp(z - A_q) <= exp(D) and pt^2 are formed
-// in fp32: rows with |D| > 32 nats (where they could overflow) get NaN.
+// in fp32: rows with |D| > 32 nats (where they could overflow) get NaN.  The
+// three terms of |p - q|^2 can cancel: for peaked distributions whose top
+// logits differ (D != 0 while p ~ q), and by ~exp(2D) when pi's lse is far
+// above mu's (r << 1).  The terms are rounded to fp32 per entry and their
+// parts added in fp64 here, so the error of the result is about 3e-7 times
+// the sum of their magnitudes: the distance is NaN where that exceeds 1 % of
+// |p - q|^2 plus 1e-8 (an error above ~1e-4 on the distance).
 constexpr int kFinRows = 32, kFinGroups = 8;
 __global__ __launch_bounds__(kFinRows * kFinGroups) void div_finalize_kernel(DivParams p) {
-  __shared__ float part_sums[5][kFinGroups][kFinRows];
+  __shared__ double part_sums[5][kFinGroups][kFinRows];
   const int rl = threadIdx.x % kFinRows, grp = threadIdx.x / kFinRows;
   const int k = blockIdx.x * kFinRows + rl;
   const bool in = k < p.rows;
   const int r = p.r0 + (in ? k : 0);
   const bool active = in && (p.mask ? p.mask[r] != 0 : true);
-  float sum[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+  double sum[5] = {0.0, 0.0, 0.0, 0.0, 0.0};  // the parts add up in fp64
   if (active) {
     const int64_t plane = (int64_t)p.n_parts * p.dp_rows;
     for (int s = grp; s < p.n_parts; s += kFinGroups)
 #pragma unroll
-      for (int c = 0; c < 5; ++c) sum[c] += p.dpart[c * plane + (int64_t)s * p.dp_rows + k];
+      for (int c = 0; c < 5; ++c) sum[c] += (double)p.dpart[c * plane + (int64_t)s * p.dp_rows + k];
   }
 #pragma unroll
   for (int c = 0; c < 5; ++c) part_sums[c][grp][rl] = sum[c];
@@ -1350,12 +1356,14 @@ __global__ __launch_bounds__(kFinRows * kFinGroups) void div_finalize_kernel(Div
       for (int g2 = 1; g2 < kFinGroups; ++g2) sum[c] += part_sums[c][g2][rl];
     }
     const float ap = merged_lse2(p.part_pi, (int64_t)p.n_strips * p.n_rows, p.n_strips, p.n_rows, r);
-    const float D = (ap - p.aq2[k]) * kLn2;
-    if (fabsf(D) <= 32.0f) {
-      const float rm1 = expm1f(-D);
-      kpm = fmaf(rm1, sum[0], sum[0]) - D;
-      kmp = sum[1] + D;
-      l2 = sqrtf(fmaxf(sum[2] + rm1 * (2.0f * sum[3] + rm1 * sum[4]), 0.0f));
+    const double D = ((double)ap - (double)p.aq2[k]) * (double)kLn2;
+    if (fabs(D) <= 32.0) {
+      const double rm1 = expm1(-D);
+      kpm = (float)(fma(rm1, sum[0], sum[0]) - D);
+      kmp = (float)(sum[1] + D);
+      const double l2sq = sum[2] + rm1 * (2.0 * sum[3] + rm1 * sum[4]);
+      const double mag = sum[2] + fabs(2.0 * rm1 * sum[3]) + rm1 * rm1 * sum[4];
+      l2 = 3e-7 * mag <= 1e-2 * l2sq + 1e-8 ? (float)sqrt(fmax(l2sq, 0.0)) : __builtin_nanf("");
     } else {
       kpm = kmp = l2 = __builtin_nanf("");
     }

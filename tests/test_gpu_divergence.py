@@ -158,3 +158,65 @@ def test_full_size_sampled_rows():
     _check(got, ref, w.d, _norms(Hs, Wh, hq_o[rows], hs_o, wq_o, ws_o, w.scaling, 1.0, range(len(rows))), rows)
     assert np.all(got["kl_pi_mu"] > 0) and np.all(got["kl_mu_pi"] > 0)
     assert np.all(got["l2"] <= np.sqrt(2 * np.minimum(got["kl_pi_mu"], got["kl_mu_pi"])) * (1 + 1e-3) + 1e-6)
+
+
+def _scaled_mu_case(T, V, d, scaling, seed, scale, pi_scale=1.0):
+    """pi's head pi_scale * W and a mu built from scale * W: the two lse differ
+    by several nats (the kernels form the measures relative to mu's lse)."""
+    H = random_bf16((T, d), seed)
+    W = random_bf16((V, d), seed + 1, std=2.5 / math.sqrt(d))
+    Wf = (W.astype(np.uint32) << 16).view(np.float32)
+    Wp = inputs.float_to_bf16_bits(Wf * np.float32(pi_scale))
+    Wm = inputs.float_to_bf16_bits(Wf * np.float32(scale))
+    hq, hs = oracle.quantize_fp8(H, scaling)
+    wq, ws = oracle.quantize_fp8(Wm, scaling)
+    return H, Wp, hq, hs, wq, ws
+
+
+def _lse_gap(H, W, hq, hs, wq, ws, scaling, rows):
+    """lse_pi - lse_mu of the rows, from the oracle's logits."""
+    from scipy.special import logsumexp
+    return np.array([logsumexp(oracle.logits_pi(H[r], W, 1.0)) -
+                     logsumexp(oracle.logits_mu(hq[r], oracle._row_scale(hs, scaling, r), wq, ws, scaling, 1.0))
+                     for r in rows])
+
+
+@pytest.mark.parametrize("scale", [1.6, 0.9])
+def test_distant_policies_match_oracle(scale):
+    # mu sharper (lse_pi - lse_mu of -3 to -6 nats) or a little flatter
+    # (+0.4 to +0.9): the terms pt = exp(z - lse_mu) are far from p, and the
+    # identities still give the oracle's values
+    T, V, d, sc = 160, 1000, 256, oracle.PER_ROW
+    H, W, hq, hs, wq, ws = _scaled_mu_case(T, V, d, sc, 21, scale)
+    ids = np.zeros(T, np.int32)
+    got = _gpu(H, W, hq, hs, wq, ws, sc, ids, 1.0)
+    ref = oracle.divergence(H, W, hq, hs, wq, ws, sc)
+    gap = _lse_gap(H, W, hq, hs, wq, ws, sc, range(T))
+    assert (gap.max() < -2.0) if scale > 1 else (0.2 < gap.min() and gap.max() < 2.0), gap
+    norms = _norms(H, W, hq, hs, wq, ws, sc, 1.0, range(T))
+    _check(got, ref, d, norms)
+
+
+def test_far_apart_policies_give_nan():
+    # |lse_pi - lse_mu| > 32: every measure is NaN (masked rows still 0)
+    T, V, d, sc = 64, 1000, 256, oracle.PER_ROW
+    torch, dev = torch_dev()
+    mask = (np.arange(T) % 4 != 1).astype(np.uint8)
+    H, W, hq, hs, wq, ws = _scaled_mu_case(T, V, d, sc, 23, 25.0)
+    assert _lse_gap(H, W, hq, hs, wq, ws, sc, range(T)).max() < -32
+    got = _gpu(H, W, hq, hs, wq, ws, sc, np.zeros(T, np.int32), 1.0, mask=up(torch, dev, mask))
+    for k in ("kl_pi_mu", "kl_mu_pi", "l2"):
+        assert np.all(np.isnan(got[k][mask == 1])), k
+        assert np.all(got[k][mask == 0] == 0), k
+    # pi's lse 5 to 8 nats above mu's: the three terms of the distance cancel
+    # beyond fp32's reach, so it is NaN; both KL stay finite and match
+    H, W, hq, hs, wq, ws = _scaled_mu_case(T, V, d, sc, 25, 0.2, pi_scale=1.6)
+    gap = _lse_gap(H, W, hq, hs, wq, ws, sc, range(T))
+    assert gap.min() > 4 and gap.max() < 32, gap
+    got = _gpu(H, W, hq, hs, wq, ws, sc, np.zeros(T, np.int32), 1.0)
+    ref = oracle.divergence(H, W, hq, hs, wq, ws, sc)
+    assert np.all(np.isnan(got["l2"]))
+    delta = 2e-4 * math.sqrt(d / 256.0)
+    for k in ("kl_pi_mu", "kl_mu_pi"):
+        tol = 1e-6 + 2 * delta * np.sqrt(2 * np.abs(ref[k])) + 1e-5 * np.abs(ref[k])
+        assert np.all(np.abs(got[k] - ref[k]) <= tol), (k, np.abs(got[k] - ref[k]).max())
