@@ -156,9 +156,10 @@ acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, vo
  * given, becomes nonzero; the flag is never cleared by the library).
  * The workspace holds a tiled copy of W, h, Wq and hq and of the E8M0 scales
  * of Wq and hq (about (3 + 1/32) (V + n_rows) d bytes) besides the per-strip
- * partial states; with packed_weights (acrl_pack_weights) the copies of W and
- * Wq come from there and the workspace holds only the activations'
- * (acrl_score_workspace_query).
+ * partial states and the work-queue counters of the persistent launches
+ * (cleared by the call itself); with packed_weights (acrl_pack_weights) the
+ * copies of W and Wq come from there and the workspace holds only the
+ * activations' (acrl_score_workspace_query).
  * policies = ACRL_POLICY_PI scores pi only (h, w, logp_pi required; the mu
  * fields are not read and the mu outputs not written), ACRL_POLICY_MU mu only;
  * the full-vocabulary measures need both.

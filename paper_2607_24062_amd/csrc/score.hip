@@ -26,6 +26,11 @@
 //    lse = ln2 (M + log2 S), entropy = ln2 (log2 S - U/S).
 //  * The strip's state per token goes to a workspace (split-V partials); a
 //    merge kernel combines the strips and writes logp = z[a_t] - lse.
+//  * The scoring launches are persistent: one workgroup per CU takes
+//    (token tile, strip) units from per-XCD queues in the workspace, its own
+//    XCD's first, so that faster XCDs take more of them.
+//  * The full-vocabulary KL / Euclidean measures fold into the pi kernel's
+//    epilogue, against mu's logits stored by mu's pass of the same rows.
 #include <algorithm>
 #include <type_traits>
 
