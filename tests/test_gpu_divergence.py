@@ -132,8 +132,11 @@ def test_lossless_operands_give_zero():
 
 
 def test_full_size_sampled_rows():
-    """d = 4096, V = 151936 (the q8b head), two passes (16384 + 300 rows):
-    sampled rows against the oracle, every row against Pinsker's bound."""
+    """d = 4096, V = 151936 (the q8b head), two passes (16384 + 300 rows): 32
+    rows against the oracle -- both ends of the call, of each pass, of a
+    256-row tile and of a 2048-row block of tiles, one row in every other
+    block, the rest seeded at random -- and every row against Pinsker's
+    bound."""
     torch, dev = torch_dev()
     from paper_2607_24062_amd import acrl
     w = inputs.WORKLOADS["q8b"]
@@ -146,7 +149,10 @@ def test_full_size_sampled_rows():
     out = acrl.acrl_score_pi_mu(Hd, Wd, hq, hs, wq, ws, w.scaling, ids, divergence=True)
     torch.cuda.synchronize()
     got = {k: down(v) for k, v in out.items()}
-    rows = np.array([0, 4097, 16383, 16384, T - 1])
+    edges = [0, 255, 256, 2047, 2048, 16383, 16384, 16385, T - 1]
+    blocks = [b * 2048 + 1000 for b in range(1, 8)]
+    rest = np.random.default_rng(31).choice(T, 32 - len(edges) - len(blocks), replace=False)
+    rows = np.unique(np.concatenate([edges, blocks, rest]))
     idx = torch.from_numpy(rows).to(dev)
     Hs = down(Hd[idx].view(torch.int16)).view(np.uint16)
     # the oracle's own quantization of the sampled rows is the GPU's (bit-exact, tested elsewhere);
