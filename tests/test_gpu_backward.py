@@ -181,9 +181,11 @@ def test_backward_slot_map_and_empty():
 
 def test_backward_full_size_sampled_rows():
     """d = 4096, V = 151936 in the bench's launch configuration (16384-row
-    passes, a ragged second pass).  Only a few rows carry a coefficient, so
-    every dW row is a sum over those tokens and the oracle can form it; dH is
-    checked on rows with and without a coefficient."""
+    passes, a ragged second pass).  40 rows carry a coefficient -- both ends
+    of each pass, of a 256-row tile and of a 2048-row block of tiles, one row
+    in every block, the rest seeded -- so every dW row is a sum over those
+    tokens and the oracle can form it; dH is checked on rows with and without
+    a coefficient."""
     torch, dev = torch_dev()
     from paper_2607_24062_amd import acrl
     w = inputs.WORKLOADS["q8b"]
@@ -191,8 +193,10 @@ def test_backward_full_size_sampled_rows():
     Hd = inputs.hidden_bf16_torch(w, T, dev)
     Wd = inputs.weights_bf16_torch(w, dev)
     r = np.random.default_rng(8)
-    live = np.sort(r.choice(T, size=6, replace=False))
-    live[-1] = T - 1  # one in the ragged tail pass
+    edges = [0, 255, 256, 2047, 2048, 16383, 16384, 16385, T - 1]  # T - 1: the ragged tail pass
+    blocks = [b * 2048 + 700 for b in range(1, 8)]
+    rest = r.choice(np.setdiff1d(np.arange(T), edges + blocks), size=40 - len(edges) - len(blocks), replace=False)
+    live = np.sort(np.concatenate([edges, blocks, rest]))
     ids = r.integers(0, V, size=T).astype(np.int32)
     coef = np.zeros(T, np.float32)
     coef[live] = r.normal(size=live.size).astype(np.float32) * 1e-3
