@@ -171,6 +171,8 @@ def main():
                     help="approximate CPU time budget of the oracle baseline (0 = skip)")
     ap.add_argument("--no-divergence", action="store_true",
                     help="skip the full-vocabulary KL / Euclidean leg")
+    ap.add_argument("--div-chunk", type=int, default=0,
+                    help="rows per pass of the full-vocabulary measures (0 = the library's 16384)")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the surrogate + LM-head backward leg")
     ap.add_argument("--no-library", action="store_true",
@@ -206,7 +208,8 @@ def main():
         del src, dst
         step(acrl, S)
         if not args.no_divergence:
-            divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["packed"], 0.0, reps=0)
+            divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["packed"], 0.0, reps=0,
+                           div_chunk=args.div_chunk)
         if not args.no_backward:
             backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["mask"], S["groups"], S["adv"], 1.0,
                          reps=0)
@@ -286,7 +289,7 @@ def main():
     score_ms = t_pi + t_mu
     if not args.no_divergence:
         line["divergence"] = divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["packed"],
-                                            score_ms)
+                                            score_ms, div_chunk=args.div_chunk)
     if not args.no_backward:
         line["backward"] = backward_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, S["mask"], S["groups"],
                                         S["adv"], S["X"])
@@ -382,7 +385,7 @@ def library_leg(torch, w, T, H, W, hq, hs, wq, ws, pi_ms, mu_ms, reps=2):
     return res if reps else None
 
 
-def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, packed, score_ms, reps=2):
+def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, packed, score_ms, reps=2, div_chunk=0):
     """The scoring call with the full-vocabulary measures (KL both ways,
     Euclidean distance) switched on: in passes of 16384 rows the mu kernel
     also stores its logits (4 B each) and the pi kernel reads them back and
@@ -394,7 +397,7 @@ def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, packed, 
     def run():
         return acrl.acrl_score_pi_mu(H, W, hq, hs, wq, ws, w.scaling, ids, inv_temperature=w.inv_temperature,
                                      out_slot=slots, n_slots=w.slots, outputs=outs, want=("entropy",),
-                                     divergence=True, packed_weights=packed)
+                                     divergence=True, div_chunk=div_chunk, packed_weights=packed)
 
     outs.update(run())
     torch.cuda.synchronize()
@@ -412,6 +415,7 @@ def divergence_leg(torch, acrl, w, T, H, W, hq, hs, wq, ws, ids, slots, packed, 
     res = {"what": "acrl_score_pi_mu with kl_pi_mu, kl_mu_pi and l2 over the batch's valid tokens",
            "ms": round(ms, 3), "score_ms_without": round(float(score_ms), 3),
            "overhead_ms": round(ms - float(score_ms), 3),
+           "rows_per_pass": div_chunk or 16384,
            "logit_bytes_stored_and_read": 2 * 4 * T * V,
            "mean_kl_pi_mu": float(kl.double().mean().item()),
            "mean_kl_mu_pi": float(outs["kl_mu_pi"][valid].double().mean().item()),

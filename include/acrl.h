@@ -171,8 +171,10 @@ acrl_status acrl_fp8_encode(const float* x, int64_t n, int rounding, void* q, vo
  *   kl_pi_mu = sum_v p_v log(p_v / q_v),  kl_mu_pi = sum_v q_v log(q_v / p_v),
  *   l2 = sqrt(sum_v (p_v - q_v)^2),
  * per row (0 for masked rows).  When any of the three is non-NULL, rows are
- * scored in passes of div_chunk rows (0 = 16384): mu's logits of a pass are
- * kept in the workspace (4 bytes per logit), and the pi kernel that follows
+ * scored in passes of at most div_chunk rows (0 = 16384; the passes that
+ * needs share the rows evenly): mu's logits of a pass are kept in the
+ * workspace (4 bytes per logit, so V * 4 bytes per row of a pass; larger
+ * passes leave fewer partly idle grid ends), and the pi kernel that follows
  * reads them back and accumulates the three measures against mu's lse; the
  * workspace must have acrl_score_div_workspace_size() bytes.  The terms are
  * formed in fp32 relative to mu's lse: rows where |lse_pi - lse_mu| > 32

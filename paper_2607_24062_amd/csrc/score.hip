@@ -1362,7 +1362,11 @@ __global__ __launch_bounds__(kFinRows * kFinGroups) void div_finalize_kernel(Div
     }
     const float ap = merged_lse2(p.part_pi, (int64_t)p.n_strips * p.n_rows, p.n_strips, p.n_rows, r);
     const double D = ((double)ap - (double)p.aq2[k]) * (double)kLn2;
-    if (fabs(D) <= 32.0) {
+    // (infinite logits leave non-finite sums)
+    bool finite = true;
+#pragma unroll
+    for (int c = 0; c < 5; ++c) finite = finite && isfinite(sum[c]);
+    if (fabs(D) <= 32.0 && finite) {
       const double rm1 = expm1(-D);
       kpm = (float)(fma(rm1, sum[0], sum[0]) - D);
       kmp = (float)(sum[1] + D);
@@ -1566,12 +1570,15 @@ ScorePlan plan_score(int64_t n_rows, int64_t d, int64_t V, int64_t div_rows, boo
   }
   // full-vocabulary measures, per pass of div_tiles token tiles: mu's
   // logits (256 KiB per pair of token and vocabulary tiles), mu's lse of the
-  // pass rows and pi's five sums per row and 128 vocabulary rows
+  // pass rows and pi's five sums per row and 128 vocabulary rows.  The
+  // passes needed at div_rows rows each share the token tiles evenly, so
+  // that no short last pass runs a grid of a few units per CU.
   pl.div_tiles = 0;
   if (div_rows > 0) {
-    const int64_t rows = std::min<int64_t>((div_rows + kTileT - 1) / kTileT * kTileT,
-                                           (int64_t)pl.n_ttiles * kTileT);
-    pl.div_tiles = (int)std::max<int64_t>(rows / kTileT, 1);
+    const int64_t req = std::max<int64_t>((div_rows + kTileT - 1) / kTileT, 1);
+    const int64_t tiles = std::max<int64_t>(pl.n_ttiles, 1);
+    const int64_t passes = (tiles + req - 1) / req;
+    pl.div_tiles = (int)((tiles + passes - 1) / passes);
     const size_t prow = (size_t)pl.div_tiles * kTileT;
     pl.ws_zbuf_offset = off;
     off += prow * pl.n_vtiles * kTileV * sizeof(float);

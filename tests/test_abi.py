@@ -114,6 +114,24 @@ def test_score_rejects_bad_arguments():
     assert nb.value >= 2 * 3 * 4 * 300
 
 
+def test_measures_passes_share_the_rows_evenly():
+    # 66 token tiles in passes of at most 64 tiles: two passes of 33, so the
+    # workspace holds mu's logits of 33 tiles, as for passes of at most 33 or
+    # 34 tiles; one pass of all 66 needs more
+    L = _acrl().lib()
+    rows, tile = 66 * 256, 256
+
+    def ws(chunk):
+        nb = ctypes.c_size_t()
+        assert L.acrl_score_div_workspace_size(rows, 256, 1000, 1, chunk, ctypes.byref(nb)) == 0
+        return nb.value
+
+    assert ws(64 * tile) == ws(33 * tile) == ws(34 * tile) == ws(64 * tile - 5)
+    # per pass row: V padded to 1024 logits, mu's lse, five sums per 128 vocabulary rows (4 B each)
+    assert ws(66 * tile) - ws(33 * tile) == 33 * tile * (1024 + 1 + 5 * 2 * 4) * 4
+    assert ws(0) == ws(16384)
+
+
 def test_reduce_and_controller_reject_bad_arguments():
     acrl = _acrl()
     L = acrl.lib()

@@ -132,8 +132,9 @@ def test_lossless_operands_give_zero():
 
 
 def test_full_size_sampled_rows():
-    """d = 4096, V = 151936 (the q8b head), two passes (16384 + 300 rows): 32
-    rows against the oracle -- both ends of the call, of each pass, of a
+    """d = 4096, V = 151936 (the q8b head), 16384 + 300 rows: two passes of
+    33 token tiles (passes of at most 16384 rows share the 66 tiles evenly).
+    32 rows against the oracle -- both ends of the call, of each pass, of a
     256-row tile and of a 2048-row block of tiles, one row in every other
     block, the rest seeded at random -- and every row against Pinsker's
     bound."""
@@ -149,7 +150,8 @@ def test_full_size_sampled_rows():
     out = acrl.acrl_score_pi_mu(Hd, Wd, hq, hs, wq, ws, w.scaling, ids, divergence=True)
     torch.cuda.synchronize()
     got = {k: down(v) for k, v in out.items()}
-    edges = [0, 255, 256, 2047, 2048, 16383, 16384, 16385, T - 1]
+    cut = 33 * 256
+    edges = [0, 255, 256, 2047, 2048, cut - 1, cut, cut + 1, 16383, 16384, T - 1]
     blocks = [b * 2048 + 1000 for b in range(1, 8)]
     rest = np.random.default_rng(31).choice(T, 32 - len(edges) - len(blocks), replace=False)
     rows = np.unique(np.concatenate([edges, blocks, rest]))
@@ -201,6 +203,51 @@ def test_distant_policies_match_oracle(scale):
     assert (gap.max() < -2.0) if scale > 1 else (0.2 < gap.min() and gap.max() < 2.0), gap
     norms = _norms(H, W, hq, hs, wq, ws, sc, 1.0, range(T))
     _check(got, ref, d, norms)
+
+
+def test_mu_logit_far_above_pi_at_one_entry():
+    # A constant input feature gives pi a large logit at entry 900 (+56) and
+    # mu one at entry 5 (+72): |lse_pi - lse_mu| of 5 to 26 nats, so the
+    # measures are defined, while at entry 5 mu's logit lies more than 44
+    # nats above every pi logit of its vocabulary tile (pi's terms there are
+    # ~2^-100 of mu's, and terms formed relative to pi's own running maximum
+    # would overflow fp32).  The values match the oracle.
+    T, V, d, sc = 64, 1000, 256, oracle.PER_ROW
+    H = random_bf16((T, d), 41)
+    W = random_bf16((V, d), 42, std=2.5 / math.sqrt(d))
+    H[:, 0] = inputs.float_to_bf16_bits(np.ones(T, np.float32))
+    Wp, Wm = W.copy(), W.copy()
+    Wp[:, 0] = 0
+    Wm[:, 0] = 0
+    Wp[900, 0] = inputs.float_to_bf16_bits(np.array([56.0], np.float32))[0]
+    Wm[5, 0] = inputs.float_to_bf16_bits(np.array([72.0], np.float32))[0]
+    hq, hs = oracle.quantize_fp8(H, sc)
+    wq, ws = oracle.quantize_fp8(Wm, sc)
+    gap = _lse_gap(H, Wp, hq, hs, wq, ws, sc, range(T))
+    assert np.all(np.abs(gap) < 32) and np.all(np.abs(gap) > 3), gap
+    from scipy.special import logsumexp
+    lse = np.zeros((2, T))
+    for r in range(T):
+        zp = oracle.logits_pi(H[r], Wp, 1.0)
+        zm = oracle.logits_mu(hq[r], oracle._row_scale(hs, sc, r), wq, ws, sc, 1.0)
+        assert zm[5] - zp[:256].max() > 45
+        lse[:, r] = logsumexp(zp), logsumexp(zm)
+    got = _gpu(H, Wp, hq, hs, wq, ws, sc, np.zeros(T, np.int32), 1.0)
+    ref = oracle.divergence(H, Wp, hq, hs, wq, ws, sc)
+    for k in ("kl_pi_mu", "kl_mu_pi", "l2"):
+        assert np.all(np.isfinite(got[k])), k
+    # Logits near 60-70 carry the matrix cores' accumulation error at their
+    # own scale (mu's lse is off by up to ~1e-2 here, against ~1e-4 at the
+    # O(1) logits the bound above assumes); each KL moves by at most the two
+    # lse errors plus the error of the logits that hold the mass, which the
+    # usual bound covers.
+    dA = np.abs(got["lse_pi"] - lse[0]) + np.abs(got["lse_mu"] - lse[1])
+    np_, nq = _norms(H, Wp, hq, hs, wq, ws, sc, 1.0, range(T))
+    delta = 2e-4 * math.sqrt(d / 256.0)
+    for k in ("kl_pi_mu", "kl_mu_pi"):
+        tol = 1e-6 + 2 * delta * np.sqrt(2 * np.abs(ref[k])) + 2 * dA
+        assert np.all(np.abs(got[k] - ref[k]) <= tol), (k, np.abs(got[k] - ref[k]).max())
+    assert np.all(np.abs(got["l2"] - ref["l2"]) <= 1e-6 + 2 * delta * (np_ + nq))
 
 
 def test_far_apart_policies_give_nan():
