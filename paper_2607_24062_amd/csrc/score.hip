@@ -581,7 +581,11 @@ void score_kernel(ScoreParams p) {
           float v[16];
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
-            v[i] = acc_read(acc[b][j][i]);
+            // (the 8-wave per-row FP8 kernels keep their accumulators in
+            // VGPRs, the MFMA's VGPR form: 12 instead of 112 bytes spilled
+            // per lane in the persistent scorer, mu 1.5-7 % faster; the other
+            // variants ran slower that way)
+            v[i] = (MODE == kFP8Row && NW == 8) ? acc[b][j][i] : acc_read(acc[b][j][i]);
             if constexpr (MODE == kFP8Row) v[i] *= rs[i];
           }
           if constexpr (EPI == kEpiSoftmaxZ) {
@@ -1140,8 +1144,7 @@ __global__ void clear_queue_kernel(int* q) { q[kQueueStride * threadIdx.x] = 0; 
 
 // Waves per workgroup of each instantiation (measured on the MI355X): two
 // per SIMD where the variant runs faster that way (the per-row FP8 scorer
-// spills 40 bytes per lane at 8 waves and is still 5-7 % faster); one per
-// SIMD otherwise.  The blockwise sampling variants fit their registers at 4
+// holds its accumulators in VGPRs there); one per SIMD otherwise.  The blockwise sampling variants fit their registers at 4
 // waves (no spills) and run as fast or faster there than at 8 (q8b 85.2 vs
 // 85.4 ms, q17b 27.0 vs 30.6 ms), where they spill around the epilogue.
 template <int MODE, int EPI>
@@ -1155,9 +1158,10 @@ constexpr int waves_for() {
 // Scoring launches: `grid` units (a multiple of kXcds).  The softmax
 // epilogues run persistent, one workgroup per CU (measured on the MI355X,
 // against one workgroup per unit, results bitwise equal: pi 5 % faster at
-// d = 4096 and 5120, 3 % at d = 2048; per-tensor FP8 mu 2.5 %, MX 1 %),
-// except the 8-wave per-row FP8 kernels, which the unit loop pushes into
-// spills (112 bytes per lane; q17b mu 4 % slower).  p.queue must point at
+// d = 4096 and 5120, 3 % at d = 2048; per-tensor FP8 mu 2.5 %, MX 1 %,
+// per-row FP8 mu 6 % at d = 2048 and 1.5 % at d = 4096), except the per-row
+// FP8 pass that stores its logits (the unit loop spills it to 104 bytes per
+// lane, and the measures call ran no faster).  p.queue must point at
 // kXcds * kQueueStride ints of workspace, cleared here.  The backward
 // products take one workgroup per unit.
 inline int device_cus() {
@@ -1172,7 +1176,7 @@ template <int MODE, int EPI>
 void launch_score_kernel(unsigned grid, const ScoreParams& p, hipStream_t s) {
   constexpr int NW = waves_for<MODE, EPI>();
   constexpr bool kPersist = (EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ || EPI == kEpiSoftmaxDiv) &&
-                            !(MODE == kFP8Row && NW == 8);
+                            !(MODE == kFP8Row && EPI == kEpiSoftmaxZ);
   if constexpr (kPersist) {
     ScoreParams q = p;
     q.units_per_xcd = (int)(grid / kXcds);
