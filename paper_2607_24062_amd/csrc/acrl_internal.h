@@ -66,6 +66,7 @@ struct BackwardPlan {
   int n_dtiles;         // hidden-dimension tiles of 256 rows
   int kch_v;            // 64-byte K chunks of a row whose K runs over the (padded) vocabulary
   size_t off_w, off_wt, off_h, off_ht, off_zt, off_zv;  // image offsets in the workspace
+  size_t off_queue;     // the products' per-XCD claim counters (persistent grid)
   size_t ws_bytes;
 };
 BackwardPlan plan_backward(int64_t n_rows, int64_t d, int64_t V, int64_t chunk);

@@ -581,11 +581,15 @@ void score_kernel(ScoreParams p) {
           float v[16];
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
-            // (the 8-wave per-row FP8 kernels keep their accumulators in
-            // VGPRs, the MFMA's VGPR form: 12 instead of 112 bytes spilled
-            // per lane in the persistent scorer, mu 1.5-7 % faster; the other
-            // variants ran slower that way)
-            v[i] = (MODE == kFP8Row && NW == 8) ? acc[b][j][i] : acc_read(acc[b][j][i]);
+            // (the 8-wave per-row FP8 kernels and the 8-wave passes of the
+            // full-vocabulary measures keep their accumulators in VGPRs, the
+            // MFMA's VGPR form: 12 instead of 112 bytes spilled per lane in
+            // the persistent per-row scorer, mu 1.5-7 % faster, and 12
+            // instead of 104 in pi's measures pass, the measures 6 ms
+            // cheaper at d = 4096; the plain BF16 and per-tensor FP8 scorers
+            // ran slower that way)
+            v[i] = ((MODE == kFP8Row || EPI == kEpiSoftmaxZ || DIV) && NW == 8) ? acc[b][j][i]
+                                                                                : acc_read(acc[b][j][i]);
             if constexpr (MODE == kFP8Row) v[i] *= rs[i];
           }
           if constexpr (EPI == kEpiSoftmaxZ) {
@@ -765,7 +769,7 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
               for (int ii = 0; ii < 4; ++ii) {
                 const int i = 4 * qq + ii;
-                const float zp = acc_read(acc[b][j][i]) * cz[j];
+                const float zp = acc[b][j][i] * cz[j];  // (VGPR form, see above)
                 float ep = fast_exp2(fmaf(zp, kLog2e, -a2[j]));
                 float eq = fast_exp2(fmaf(zq[i], kLog2e, -a2[j]));
                 if constexpr (kTail) {
@@ -890,7 +894,7 @@ void score_kernel(ScoreParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int m = m0 + 32 * b + 8 * (i >> 2) + (i & 3);
-          const float x = acc_read(acc[b][j][i]);
+          const float x = acc[b][j][i];  // (VGPR form: the 8-wave products)
           if (m < p.c_rows && tok[j] < p.n_rows) p.c[(int64_t)m * p.ldc + tok[j]] = x;
         }
   };
@@ -1143,14 +1147,17 @@ void score_kernel(ScoreParams p) {
 __global__ void clear_queue_kernel(int* q) { q[kQueueStride * threadIdx.x] = 0; }
 
 // Waves per workgroup of each instantiation (measured on the MI355X): two
-// per SIMD where the variant runs faster that way (the per-row FP8 scorer
-// holds its accumulators in VGPRs there); one per SIMD otherwise.  The blockwise sampling variants fit their registers at 4
-// waves (no spills) and run as fast or faster there than at 8 (q8b 85.2 vs
-// 85.4 ms, q17b 27.0 vs 30.6 ms), where they spill around the epilogue.
+// per SIMD where the variant runs faster that way (the per-row FP8 scorer,
+// the measures' passes and the backward's plain products hold their
+// accumulators in VGPRs there); one per SIMD otherwise.  The blockwise
+// sampling variants fit their registers at 4 waves (no spills) and run as
+// fast or faster there than at 8 (q8b 85.2 vs 85.4 ms, q17b 27.0 vs
+// 30.6 ms), where they spill around the epilogue; the dZ pass spills at 8.
 template <int MODE, int EPI>
 constexpr int waves_for() {
   return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) ||
-          (EPI == kEpiSoftmaxZ && (MODE == kFP8Tensor || MODE == kFP8Row)) || (EPI == kEpiSoftmaxDiv && MODE == kBF16))
+          (EPI == kEpiSoftmaxZ && (MODE == kFP8Tensor || MODE == kFP8Row)) ||
+          (EPI == kEpiSoftmaxDiv && MODE == kBF16) || EPI == kEpiStore)
              ? 8
              : 4;
 }
@@ -1162,8 +1169,10 @@ constexpr int waves_for() {
 // per-row FP8 mu 6 % at d = 2048 and 1.5 % at d = 4096), except the per-row
 // FP8 pass that stores its logits (the unit loop spills it to 104 bytes per
 // lane, and the measures call ran no faster).  p.queue must point at
-// kXcds * kQueueStride ints of workspace, cleared here.  The backward
-// products take one workgroup per unit.
+// kXcds * kQueueStride ints of workspace, cleared here.  The backward's
+// plain products run persistent too (8 waves, VGPR accumulators: the q8b
+// backward 502 -> 490 ms, of which ~1 ms from the persistent grid); its dZ
+// pass takes one workgroup per unit (no faster persistent).
 inline int device_cus() {
   int dev = 0, n = 0;
   if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -1175,7 +1184,8 @@ inline int device_cus() {
 template <int MODE, int EPI>
 void launch_score_kernel(unsigned grid, const ScoreParams& p, hipStream_t s) {
   constexpr int NW = waves_for<MODE, EPI>();
-  constexpr bool kPersist = (EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ || EPI == kEpiSoftmaxDiv) &&
+  constexpr bool kPersist = (EPI == kEpiSoftmax || EPI == kEpiSample || EPI == kEpiSoftmaxZ || EPI == kEpiSoftmaxDiv ||
+                             EPI == kEpiStore) &&
                             !(MODE == kFP8Row && EPI == kEpiSoftmaxZ);
   if constexpr (kPersist) {
     ScoreParams q = p;
@@ -1746,7 +1756,7 @@ hipError_t launch_score(const acrl_score_desc& dsc, const ScorePlan& pl, hipStre
 }
 
 // ------------------------------------------------------------------ backward
-// Grid of a plain product (kEpiStore): one workgroup per output tile, in the
+// Grid of a plain product (kEpiStore): one unit per output tile, in the
 // scoring kernel's XCD-aware raster (A tiles play the vocabulary strips, B
 // tiles the token tiles).
 static void gemm_grid(int n_atiles, int n_btiles, ScoreParams& pp, unsigned& grid) {
@@ -1783,6 +1793,7 @@ BackwardPlan plan_backward(int64_t n_rows, int64_t d, int64_t V, int64_t chunk) 
   pl.off_ht = take(drows * crows * 2);                     // H^T chunk, rows = d, K = tokens
   pl.off_zt = take((size_t)n_ttiles * kTileT * vrows * 2); // dZ, rows = tokens, K = vocabulary
   pl.off_zv = take(vrows * crows * 2);                     // dZ^T, rows = vocabulary, K = tokens
+  pl.off_queue = take((size_t)kXcds * kQueueStride * sizeof(int));  // the products' claim counters
   pl.ws_bytes = off;
   return pl;
 }
@@ -1865,6 +1876,7 @@ hipError_t launch_backward(const acrl_backward_desc& dsc, const BackwardPlan& pl
       pc.ldc = d;
       pc.c_rows = (int)rows;
       pc.c_accumulate = 0;
+      pc.queue = reinterpret_cast<int*>(ws + pl.off_queue);
       launch_score_kernel<kBF16, kEpiStore>(grid, pc, s);
     }
     // dW (+)= dZ^T H: A = dZ^T (rows = vocabulary), B = H^T (rows = d), K = tokens
@@ -1881,6 +1893,7 @@ hipError_t launch_backward(const acrl_backward_desc& dsc, const BackwardPlan& pl
       pc.ldc = d;
       pc.c_rows = (int)V;
       pc.c_accumulate = (r0 > 0 || dsc.accumulate_dw) ? 1 : 0;
+      pc.queue = reinterpret_cast<int*>(ws + pl.off_queue);
       launch_score_kernel<kBF16, kEpiStore>(grid, pc, s);
     }
   }
