@@ -476,7 +476,8 @@ acrl_status acrl_surrogate(const acrl_surrogate_desc* desc, void* stream);
  * up to a multiple of 256; at most 2^23); workspace of
  * acrl_backward_workspace_size() bytes (packed W, W^T, one chunk of H, H^T
  * and two bf16 copies of its dZ: about 4 V d + 4 c d + 4 c V bytes for a
- * chunk of c rows).                                                         */
+ * chunk of c rows; plus the products' work-queue counters, cleared by the
+ * call).                                                                    */
 typedef struct acrl_backward_desc {
   int64_t n_rows;
   int64_t d;
