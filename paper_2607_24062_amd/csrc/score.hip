@@ -581,16 +581,15 @@ void score_kernel(ScoreParams p) {
           float v[16];
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
-            // (the 8-wave per-row FP8 kernels, the 8-wave passes of the
-            // full-vocabulary measures and the 8-wave draws keep their
-            // accumulators in VGPRs, the MFMA's VGPR form: 12 instead of 112
-            // bytes spilled per lane in the persistent per-row scorer, mu
-            // 1.5-7 % faster, and 12 instead of 104 in pi's measures pass,
-            // the measures 6 ms cheaper at d = 4096; the draws 1-5 % faster
-            // than at 4 waves; the plain BF16 and per-tensor FP8 scorers ran
-            // slower that way)
-            v[i] = ((MODE == kFP8Row || EPI == kEpiSoftmaxZ || DIV || SAMPLE) && NW == 8) ? acc[b][j][i]
-                                                                                          : acc_read(acc[b][j][i]);
+            // (the 8-wave per-row FP8 kernels and the 8-wave passes of the
+            // full-vocabulary measures keep their accumulators in VGPRs, the
+            // MFMA's VGPR form: 12 instead of 112 bytes spilled per lane in
+            // the persistent per-row scorer, mu 1.5-7 % faster, and 12
+            // instead of 104 in pi's measures pass, the measures 6 ms
+            // cheaper at d = 4096; the plain BF16 and per-tensor FP8 scorers
+            // ran slower that way)
+            v[i] = ((MODE == kFP8Row || EPI == kEpiSoftmaxZ || DIV) && NW == 8) ? acc[b][j][i]
+                                                                                : acc_read(acc[b][j][i]);
             if constexpr (MODE == kFP8Row) v[i] *= rs[i];
           }
           if constexpr (EPI == kEpiSoftmaxZ) {
@@ -1149,17 +1148,14 @@ __global__ void clear_queue_kernel(int* q) { q[kQueueStride * threadIdx.x] = 0; 
 
 // Waves per workgroup of each instantiation (measured on the MI355X): two
 // per SIMD where the variant runs faster that way (the per-row FP8 scorer,
-// the measures' passes, the per-tensor and per-row draws and the
-// backward's plain products hold their accumulators in VGPRs there); one
-// per SIMD otherwise.  The draws with AGPR accumulators fit their registers
-// at 4 waves and ran as fast or faster there than at 8; with VGPR
-// accumulators at 8 waves they run 1 % (q8b) and 5 % (q17b) faster than at
-// 4, although the per-row one spills.  The MX draw and the dZ pass spill
-// more at 8.
+// the measures' passes and the backward's plain products hold their
+// accumulators in VGPRs there); one per SIMD otherwise.  The blockwise
+// sampling variants fit their registers at 4 waves (no spills) and run as
+// fast or faster there than at 8 (q8b 85.2 vs 85.4 ms, q17b 27.0 vs
+// 30.6 ms), where they spill around the epilogue; the dZ pass spills at 8.
 template <int MODE, int EPI>
 constexpr int waves_for() {
   return ((EPI == kEpiSoftmax && (MODE == kBF16 || MODE == kFP8Tensor || MODE == kFP8Row)) ||
-          (EPI == kEpiSample && (MODE == kFP8Tensor || MODE == kFP8Row)) ||
           (EPI == kEpiSoftmaxZ && (MODE == kFP8Tensor || MODE == kFP8Row)) ||
           (EPI == kEpiSoftmaxDiv && MODE == kBF16) || EPI == kEpiStore)
              ? 8
