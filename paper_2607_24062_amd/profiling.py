@@ -15,6 +15,7 @@ Command line:
     python -m paper_2607_24062_amd.profiling stats CSV TITLE COMMAND > profiles/x.md
     python -m paper_2607_24062_amd.profiling traffic FETCH_CSV WRITE_CSV TITLE COMMAND > profiles/y.md
     python -m paper_2607_24062_amd.profiling trace TRACE_CSV TITLE COMMAND [PREFIX] > profiles/z.md
+    python -m paper_2607_24062_amd.profiling counters COUNTER_CSV TITLE COMMAND > profiles/w.md
 """
 from __future__ import annotations
 
@@ -201,6 +202,26 @@ def per_cu_markdown(counter_csv: str, title: str, command: str) -> str:
     return "\n".join(lines) + "\n"
 
 
+def counters_markdown(counter_csv: str, title: str, command: str) -> str:
+    """Per-dispatch mean of every counter of one --pmc pass, by kernel."""
+    names, table = [], {}
+    with open(counter_csv) as f:
+        for r in csv.DictReader(f):
+            c = r["Counter_Name"]
+            if c not in names:
+                names.append(c)
+            d = table.setdefault(short_name(r["Kernel_Name"]), {})
+            d.setdefault(c, []).append(float(r["Counter_Value"]))
+    out = ["# %s" % title, "", "Command (from the repository root on one MI355X):", "", "```", command, "```", "",
+           "Per-dispatch means.", "", "| kernel | dispatches | " + " | ".join(names) + " |",
+           "|---|---|" + "---|" * len(names)]
+    for k in sorted(table, key=lambda k: -max(sum(v) / len(v) for v in table[k].values())):
+        n = max(len(v) for v in table[k].values())
+        cells = ["%.4g" % (sum(table[k][c]) / len(table[k][c])) if c in table[k] else "" for c in names]
+        out.append("| %s | %d | %s |" % (k, n, " | ".join(cells)))
+    return "\n".join(out) + "\n"
+
+
 def trace_rows(trace_csv: str, prefix: str = ""):
     """Per (kernel, launch size) from a --kernel-trace CSV: calls, mean,
     min and max duration (ms), for the kernels whose short name starts with
@@ -228,6 +249,9 @@ def trace_markdown(trace_csv: str, title: str, command: str, prefix: str = "") -
 def main(argv):
     if len(argv) >= 4 and argv[0] == "trace":
         sys.stdout.write(trace_markdown(argv[1], argv[2], argv[3], argv[4] if len(argv) > 4 else ""))
+        return 0
+    if len(argv) >= 4 and argv[0] == "counters":
+        sys.stdout.write(counters_markdown(argv[1], argv[2], argv[3]))
         return 0
     if len(argv) >= 4 and argv[0] == "percu":
         sys.stdout.write(per_cu_markdown(argv[1], argv[2], argv[3]))
