@@ -56,9 +56,9 @@ def _gpu(H, W, hq, hs, wq, ws, scaling, ids, tau, **kw):
     return {k: down(v) for k, v in out.items()}
 
 
-def _check(got, ref, d, norms, rows=None):
+def _check(got, ref, d, norms, rows=None, tau=1.0):
     sel = slice(None) if rows is None else rows
-    delta = 2e-4 * math.sqrt(d / 256.0)
+    delta = 2e-4 * math.sqrt(d / 256.0) / tau  # the logits carry 1/tau
     np_, nq = norms
     for k in ("kl_pi_mu", "kl_mu_pi", "l2"):
         g, r = got[k][sel], ref[k]
@@ -166,6 +166,42 @@ def test_full_size_sampled_rows():
     _check(got, ref, w.d, _norms(Hs, Wh, hq_o[rows], hs_o, wq_o, ws_o, w.scaling, 1.0, range(len(rows))), rows)
     assert np.all(got["kl_pi_mu"] > 0) and np.all(got["kl_mu_pi"] > 0)
     assert np.all(got["l2"] <= np.sqrt(2 * np.minimum(got["kl_pi_mu"], got["kl_mu_pi"])) * (1 + 1e-3) + 1e-6)
+
+
+@pytest.mark.parametrize("name", ["q17b", "mx"])
+def test_full_size_other_heads(name):
+    """The 1.7B-shaped head with per-row FP8 (d = 2048) and the MXFP8 head
+    (d = 5120, tau = 0.7) at V = 151936: 4096 + 300 rows in passes of at
+    most 2048 rows (three passes of 6 token tiles), 24 rows against the
+    oracle -- both ends of the call and of each pass, a tile edge, the rest
+    seeded at random."""
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    w = inputs.WORKLOADS[name]
+    tau = 1.0 / w.inv_temperature
+    T = 4096 + 300
+    Hd = inputs.hidden_bf16_torch(w, T, dev)
+    Wd = inputs.weights_bf16_torch(w, dev)
+    hq, hs = acrl.acrl_quantize_fp8(Hd, w.scaling)
+    wq, ws = acrl.acrl_quantize_fp8(Wd, w.scaling)
+    ids = torch.zeros(T, dtype=torch.int32, device=dev)
+    out = acrl.acrl_score_pi_mu(Hd, Wd, hq, hs, wq, ws, w.scaling, ids, inv_temperature=w.inv_temperature,
+                                divergence=True, div_chunk=2048)
+    torch.cuda.synchronize()
+    got = {k: down(v) for k, v in out.items()}
+    cut = 6 * 256
+    edges = [0, 255, 256, cut - 1, cut, 2 * cut - 1, 2 * cut, T - 1]
+    rest = np.random.default_rng(37).choice(T, 24 - len(edges), replace=False)
+    rows = np.unique(np.concatenate([edges, rest]))
+    idx = torch.from_numpy(rows).to(dev)
+    Hs = down(Hd[idx].view(torch.int16)).view(np.uint16)
+    # the oracle's own quantization of the sampled rows (per-row and MX scales are per row)
+    hq_o, hs_o = oracle.quantize_fp8(Hs, w.scaling)
+    Wh = down(Wd.view(torch.int16)).view(np.uint16)
+    wq_o, ws_o = oracle.quantize_fp8(Wh, w.scaling)
+    ref = oracle.divergence(Hs, Wh, hq_o, hs_o, wq_o, ws_o, w.scaling, inv_temperature=w.inv_temperature)
+    _check(got, ref, w.d, _norms(Hs, Wh, hq_o, hs_o, wq_o, ws_o, w.scaling, tau, range(len(rows))), rows, tau=tau)
+    assert np.all(got["kl_pi_mu"] > 0) and np.all(got["kl_mu_pi"] > 0)
 
 
 def _scaled_mu_case(T, V, d, scaling, seed, scale, pi_scale=1.0):
