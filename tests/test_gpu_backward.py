@@ -215,6 +215,44 @@ def test_backward_full_size_sampled_rows():
     assert np.all(down(dh[torch.from_numpy(dead).to(dev)]) == 0)
 
 
+@pytest.mark.parametrize("name", ["q17b", "mx"])
+def test_backward_other_heads_sampled_rows(name):
+    """The 1.7B-shaped head (d = 2048) and the d = 5120 head at tau = 0.7,
+    V = 151936: 4096 + 300 rows in passes of 2048 (three passes, the last
+    ragged).  24 rows carry a coefficient -- both ends of the call, of each
+    pass and of a tile, the rest seeded -- and the oracle forms dH on them
+    and dW on the rows they touch and a few others."""
+    torch, dev = torch_dev()
+    from paper_2607_24062_amd import acrl
+    w = inputs.WORKLOADS[name]
+    tau = 1.0 / w.inv_temperature
+    T, d, V = 4096 + 300, w.d, w.V
+    Hd = inputs.hidden_bf16_torch(w, T, dev)
+    Wd = inputs.weights_bf16_torch(w, dev)
+    r = np.random.default_rng(9)
+    edges = [0, 255, 256, 2047, 2048, 4095, 4096, T - 1]
+    rest = r.choice(np.setdiff1d(np.arange(T), edges), size=24 - len(edges), replace=False)
+    live = np.sort(np.concatenate([edges, rest]))
+    ids = r.integers(0, V, size=T).astype(np.int32)
+    coef = np.zeros(T, np.float32)
+    coef[live] = r.normal(size=live.size).astype(np.float32) * 1e-3
+    Hl = down(Hd[torch.from_numpy(live).to(dev)].view(torch.int16)).view(np.uint16)
+    Wh = down(Wd.view(torch.int16)).view(np.uint16)
+    lse = np.zeros(T, np.float32)
+    lse[live] = [oracle.token_stats(oracle.logits_pi(Hl[k], Wh, 1.0 / tau), int(ids[t]))[0]
+                 for k, t in enumerate(live)]
+    dh, dw = acrl.acrl_lm_head_backward(Hd, Wd, up(torch, dev, ids), up(torch, dev, coef), up(torch, dev, lse),
+                                        inv_temperature=1.0 / tau, token_chunk=2048)
+    torch.cuda.synchronize()
+    wrows = np.concatenate([np.unique(ids[live]), r.choice(V, size=6, replace=False), [V - 1]])
+    rdh, rdw, rdha, rdwa = oracle.lm_head_backward(Hl, Wh, ids[live], coef[live].astype(np.float64), 1.0 / tau,
+                                                   wrows=wrows, want_abs=True)
+    _check_rows(down(dh[torch.from_numpy(live).to(dev)]), rdh, rdha, "dH (%s)" % name)
+    _check_rows(down(dw[torch.from_numpy(wrows).to(dev)]), rdw, rdwa, "dW (%s)" % name)
+    dead = np.setdiff1d(np.arange(0, T, 331), live)
+    assert np.all(down(dh[torch.from_numpy(dead).to(dev)]) == 0)
+
+
 def test_chain_score_surrogate_backward_small_workload():
     """The small workload end to end: the GPU's own log-probs and lse feed its
     surrogate and backward; the oracle runs its own chain on the same inputs.
