@@ -12,6 +12,12 @@ def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
 
 
+def pytest_runtest_logfinish(nodeid, location):
+    # the progress mark of every finished test reaches a piped stdout at once
+    # (block buffering would hold it back for the whole run)
+    sys.stdout.flush()
+
+
 @pytest.fixture(scope="session", autouse=True)
 def _oracle_built():
     import oracle

@@ -26,3 +26,15 @@ def down(t) -> np.ndarray:
 
 def bf16_bits(t) -> np.ndarray:
     return t.detach().cpu().view(dtype=__import__("torch").int16).numpy().view(np.uint16)
+
+
+def par_map(fn, items):
+    """fn over items on a pool of threads, results in order.  For the
+    oracle's one-row calls: ctypes releases the GIL while the C runs, so the
+    rows proceed on separate cores (the oracle's functions share no state)."""
+    import os
+    from concurrent.futures import ThreadPoolExecutor
+    items = list(items)
+    workers = max(1, min(16, os.cpu_count() or 1, len(items)))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        return list(ex.map(fn, items))

@@ -16,7 +16,7 @@ import pytest
 import inputs
 import oracle
 from cases import random_bf16, workload_case
-from gpu_util import down, torch_dev, up, up_bf16
+from gpu_util import down, par_map, torch_dev, up, up_bf16
 
 pytestmark = pytest.mark.gpu
 
@@ -203,7 +203,9 @@ def test_backward_full_size_sampled_rows():
     Hl = down(Hd[torch.from_numpy(live).to(dev)].view(torch.int16)).view(np.uint16)
     Wh = down(Wd.view(torch.int16)).view(np.uint16)
     lse = np.zeros(T, np.float32)
-    lse[live] = [oracle.token_stats(oracle.logits_pi(Hl[k], Wh, 1.0), int(ids[t]))[0] for k, t in enumerate(live)]
+    oracle.lib()
+    lse[live] = par_map(lambda kt: oracle.token_stats(oracle.logits_pi(Hl[kt[0]], Wh, 1.0), int(ids[kt[1]]))[0],
+                        enumerate(live))
     dh, dw = acrl.acrl_lm_head_backward(Hd, Wd, up(torch, dev, ids), up(torch, dev, coef), up(torch, dev, lse))
     torch.cuda.synchronize()
     wrows = np.concatenate([np.unique(ids[live]), r.choice(V, size=6, replace=False), [V - 1]])
@@ -239,8 +241,9 @@ def test_backward_other_heads_sampled_rows(name):
     Hl = down(Hd[torch.from_numpy(live).to(dev)].view(torch.int16)).view(np.uint16)
     Wh = down(Wd.view(torch.int16)).view(np.uint16)
     lse = np.zeros(T, np.float32)
-    lse[live] = [oracle.token_stats(oracle.logits_pi(Hl[k], Wh, 1.0 / tau), int(ids[t]))[0]
-                 for k, t in enumerate(live)]
+    oracle.lib()
+    lse[live] = par_map(lambda kt: oracle.token_stats(oracle.logits_pi(Hl[kt[0]], Wh, 1.0 / tau),
+                                                      int(ids[kt[1]]))[0], enumerate(live))
     dh, dw = acrl.acrl_lm_head_backward(Hd, Wd, up(torch, dev, ids), up(torch, dev, coef), up(torch, dev, lse),
                                         inv_temperature=1.0 / tau, token_chunk=2048)
     torch.cuda.synchronize()

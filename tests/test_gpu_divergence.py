@@ -21,20 +21,22 @@ from scipy.special import softmax
 import inputs
 import oracle
 from cases import lossless_integer_case, random_bf16
-from gpu_util import down, torch_dev, up, up_bf16
+from gpu_util import down, par_map, torch_dev, up, up_bf16
 
 pytestmark = pytest.mark.gpu
 
 
 def _norms(H, W, hq, hs, wq, ws, scaling, tau, rows):
     """|p|_2 and |q|_2 of the rows, from the oracle's logits."""
-    npn, nqn = [], []
-    for r in rows:
+    oracle.lib()
+
+    def one(r):
         zp = oracle.logits_pi(H[r], W, 1.0 / tau)
         zm = oracle.logits_mu(hq[r], oracle._row_scale(hs, scaling, r), wq, ws, scaling, 1.0 / tau)
-        npn.append(np.linalg.norm(softmax(zp)))
-        nqn.append(np.linalg.norm(softmax(zm)))
-    return np.array(npn), np.array(nqn)
+        return np.linalg.norm(softmax(zp)), np.linalg.norm(softmax(zm))
+
+    nrm = np.array(par_map(one, rows)).reshape(-1, 2)
+    return nrm[:, 0], nrm[:, 1]
 
 
 def _case(T, V, d, scaling, seed):
