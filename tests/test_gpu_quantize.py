@@ -133,26 +133,30 @@ def test_encoder_exhaustive_fp32(rounding, chunk):
                              % (lo + i, qg[i], qo[i]))
 
 
+@pytest.mark.parametrize("operand", ["W", "H"])
+@pytest.mark.parametrize("rounding", ROUNDINGS)
 @pytest.mark.parametrize("name,scaling", [("q8b", oracle.PER_TENSOR), ("q17b", oracle.PER_ROW),
                                           ("mx", oracle.MX32)])
-def test_full_size_lm_head_sampled_rows(name, scaling):
-    """Full-size W on the device (as the benchmark quantizes it); sampled rows
-    checked bit-exactly.  For per-tensor scaling the sample includes the row
-    holding the global maximum, so the oracle derives the same scale."""
+def test_full_size_lm_head_sampled_rows(name, scaling, rounding, operand):
+    """Full-size W and H on the device (as the benchmark quantizes them), both
+    roundings; sampled rows checked bit-exactly.  For per-tensor scaling the
+    sample includes the row holding the global maximum, so the oracle derives
+    the same scale."""
     torch, dev = torch_dev()
     from paper_2607_24062_amd import acrl
     w = inputs.WORKLOADS[name]
-    W = inputs.weights_bf16_torch(w, dev)
-    q, s = acrl.acrl_quantize_fp8(W, scaling)
+    X = inputs.weights_bf16_torch(w, dev) if operand == "W" else inputs.hidden_bf16_torch(w, inputs.n_valid(w), dev)
+    q, s = acrl.acrl_quantize_fp8(X, scaling, rounding=rounding)
     torch.cuda.synchronize()
-    rows = np.random.default_rng(0).choice(w.V, size=24, replace=False)
-    rows = np.unique(np.concatenate([rows, [0, w.V - 1]]))
+    n = X.shape[0]
+    rows = np.random.default_rng(0).choice(n, size=24, replace=False)
+    rows = np.unique(np.concatenate([rows, [0, n - 1]]))
     if scaling == oracle.PER_TENSOR:
-        amax_row = int(torch.argmax(W.abs().float().amax(dim=1)).item())
+        amax_row = int(torch.argmax(X.abs().float().amax(dim=1)).item())
         rows = np.unique(np.concatenate([rows, [amax_row]]))
     idx = torch.from_numpy(rows).to(dev)
-    Wb = W.index_select(0, idx).cpu().view(torch.int16).numpy().view(np.uint16)
-    qo, so = oracle.quantize_fp8(Wb, scaling)
+    Xb = X.index_select(0, idx).cpu().view(torch.int16).numpy().view(np.uint16)
+    qo, so = oracle.quantize_fp8(Xb, scaling, rounding=rounding)
     qg = down(q.index_select(0, idx))
     assert np.array_equal(qg, qo)
     if scaling == oracle.PER_TENSOR:
@@ -161,7 +165,7 @@ def test_full_size_lm_head_sampled_rows(name, scaling):
         assert np.array_equal(down(s)[rows].view(np.uint8), so.view(np.uint8))
     else:
         assert np.array_equal(down(s)[rows], so)
-    del W, q, s
+    del X, q, s
     torch.cuda.empty_cache()
 
 
